@@ -1,0 +1,149 @@
+"""ctypes wrapper of the CPU oracle library ``libntc_oracle.so``.
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+benchmark's CPU-baseline leg.  The product package never imports this module.
+Each wrapper restates the definition it evaluates; the C source cites the
+paper passages.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "ntc_oracle.c")
+LIB = os.path.join(HERE, "libntc_oracle.so")
+PAD = 0xFFFFFFFF
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (IEEE double, no contraction, OpenMP)."""
+    if force or not os.path.exists(LIB):
+        tmp = LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+                               "-ffp-contract=off", "-fno-fast-math", "-Wall", "-o", tmp, SRC,
+                               "-lm"])
+        os.replace(tmp, LIB)
+    return LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build(force=False)
+        L = ctypes.CDLL(LIB)
+        P = ctypes.c_void_p
+        i32, i64 = ctypes.c_int32, ctypes.c_int64
+        L.ntc_oracle_build_bins.argtypes = [P, i64, P, i32, i32, i32, P, P, P, i64, P]
+        L.ntc_oracle_divergence.argtypes = [P, i64, P, i32, i32, P, i64, i32, P, P]
+        L.ntc_oracle_features.argtypes = [P, i32, i32, P, P, P, P, P, i64, P, i64, i32, P]
+        L.ntc_oracle_decode.argtypes = [P, i32, i32, P, P, P, i32, i32, P, P, P, P, P, i64, P,
+                                        i64, i32, P]
+        L.ntc_oracle_half_to_double.argtypes = [ctypes.c_uint16]
+        L.ntc_oracle_half_to_double.restype = ctypes.c_double
+        for f in ("ntc_oracle_build_bins", "ntc_oracle_divergence", "ntc_oracle_features",
+                  "ntc_oracle_decode"):
+            getattr(L, f).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def _u32(a):
+    return np.ascontiguousarray(a, dtype=np.uint32)
+
+
+def default_threads() -> int:
+    return len(os.sched_getaffinity(0))
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def build_bins(tex_id, tex_to_dec, n_decoders, align=64, n_textures=None, capacity=None):
+    """Stable counting sort of queries by decoder id -> (bin_count, bin_offset, perm, n_invalid).
+
+    perm is trimmed to bin_offset[-1] entries.
+    """
+    tex_id, tex_to_dec = _u32(tex_id), _u32(tex_to_dec)
+    n = tex_id.shape[0]
+    T = tex_to_dec.shape[0] if n_textures is None else n_textures
+    cap = n + n_decoders * (align - 1) if capacity is None else capacity
+    cnt = np.zeros(n_decoders, np.uint32)
+    off = np.zeros(n_decoders + 1, np.uint32)
+    perm = np.zeros(max(cap, 1), np.uint32)
+    bad = np.zeros(1, np.int64)
+    rc = lib().ntc_oracle_build_bins(_p(tex_id), n, _p(tex_to_dec), T, n_decoders, align,
+                                     _p(cnt), _p(off), _p(perm), cap, _p(bad))
+    if rc != 0:
+        raise OracleError("ntc_oracle_build_bins -> %d" % rc)
+    return cnt, off, perm[: int(off[-1])].copy(), int(bad[0])
+
+
+def divergence(tex_id, tex_to_dec, n_decoders, order=None, wave=64, n_textures=None):
+    """Distinct decoder ids per window of `wave` entries -> (per_wave, totals[4])."""
+    tex_id, tex_to_dec = _u32(tex_id), _u32(tex_to_dec)
+    n = tex_id.shape[0]
+    T = tex_to_dec.shape[0] if n_textures is None else n_textures
+    if order is not None:
+        order = _u32(order)
+    ln = n if order is None else order.shape[0]
+    per = np.zeros(max(1, (ln + wave - 1) // wave), np.uint32)
+    tot = np.zeros(4, np.uint64)
+    rc = lib().ntc_oracle_divergence(_p(tex_id), n, _p(tex_to_dec), T, n_decoders, _p(order), ln,
+                                     wave, _p(per), _p(tot))
+    if rc != 0:
+        raise OracleError("ntc_oracle_divergence -> %d" % rc)
+    return per[: (ln + wave - 1) // wave], tot
+
+
+def _grid_args(w):
+    res = np.ascontiguousarray(w.res, dtype=np.int32)
+    ch = np.ascontiguousarray(w.channels, dtype=np.int32)
+    return res, ch
+
+
+def features(w, subset=None, threads=None, fill=np.nan):
+    """Concatenated per-level latent samples of each query (rows of invalid queries = fill)."""
+    res, ch = _grid_args(w)
+    F = int(sum(w.channels))
+    sub = None if subset is None else np.ascontiguousarray(subset, dtype=np.int64)
+    n_sel = w.n if sub is None else sub.shape[0]
+    out = np.full((n_sel, F), fill, np.float64)
+    rc = lib().ntc_oracle_features(_p(w.latents), w.n_textures, w.n_levels, _p(res), _p(ch),
+                                   _p(w.tex_id), _p(w.uv), _p(w.mip), w.n, _p(sub), n_sel,
+                                   threads or default_threads(), _p(out))
+    if rc != 0:
+        raise OracleError("ntc_oracle_features -> %d" % rc)
+    return out
+
+
+def decode(w, subset=None, threads=None, fill=np.nan):
+    """Decoded channels of each query (rows of invalid queries = fill)."""
+    res, ch = _grid_args(w)
+    dims = np.ascontiguousarray(w.dims, dtype=np.int32)
+    sub = None if subset is None else np.ascontiguousarray(subset, dtype=np.int64)
+    n_sel = w.n if sub is None else sub.shape[0]
+    out = np.full((n_sel, w.out_dim), fill, np.float64)
+    rc = lib().ntc_oracle_decode(_p(w.latents), w.n_textures, w.n_levels, _p(res), _p(ch),
+                                 _p(w.params), w.n_decoders, w.n_layers, _p(dims),
+                                 _p(w.tex_to_dec), _p(w.tex_id), _p(w.uv), _p(w.mip), w.n,
+                                 _p(sub), n_sel, threads or default_threads(), _p(out))
+    if rc != 0:
+        raise OracleError("ntc_oracle_decode -> %d" % rc)
+    return out
+
+
+def half_to_double(bits: int) -> float:
+    return lib().ntc_oracle_half_to_double(bits)

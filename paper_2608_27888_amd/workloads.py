@@ -1,0 +1,368 @@
+"""Seeded synthetic inputs for neural texture decode.
+
+This module only *draws* inputs: latent grids, decoder parameters, the
+texture -> decoder map and the texel query stream.  It holds none of the decode
+arithmetic (no sampling, no MLP, no binning), so both the HIP path and the CPU
+oracle can be fed from it without sharing any of the method's code.
+
+Shapes follow the neural-texture-compression setting of the paper (Sec. 1 and
+Sec. 4 "Results"): every texture owns a small multi-resolution latent grid, a
+decoder MLP is chosen per texture through the map c(i) (Alg. "Overall texture
+processing pipeline", Stage 2), and the renderer issues one query per pixel
+sample.  The paper's data (Polyhaven textures, the three rendered scenes, the
+trained networks) is not available, so every array here is synthetic:
+
+* latents ~ N(0, 1), stored as fp16 (the paper decodes in FP16, Sec. 4.4);
+* weights Kaiming-uniform, bound sqrt(6 / fan_in); biases U(-0.1, 0.1); fp16;
+* screen-space query streams in row-major pixel order with per-sample jitter;
+* material layouts either per 8x8 tile or a Voronoi map of seeded regions.
+
+Every component draws from its own child of ``numpy.random.SeedSequence(seed)``
+(latents, decoders, map, queries), so a variant with a different decoder count
+shares latents and queries with its base workload.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Optional
+
+import numpy as np
+
+# Child-stream indices of the seed sequence, one per drawn component.
+_STREAM_LATENTS, _STREAM_DECODERS, _STREAM_MAP, _STREAM_QUERIES, _STREAM_LAYOUT = range(5)
+
+F32_BELOW_ONE = np.nextafter(np.float32(1.0), np.float32(0.0))
+
+
+def _rng(seed: int, stream: int) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence(seed).spawn(8)[stream])
+
+
+@dataclass
+class Workload:
+    """One decode problem: grids, decoders, map and queries (host arrays)."""
+
+    name: str
+    # latent grids (uniform across textures)
+    n_textures: int
+    res: list                    # per level: square resolution
+    channels: list               # per level: channels per texel
+    latents: np.ndarray          # uint16 fp16 bits, [T * texture_stride]
+    # decoders
+    n_decoders: int
+    dims: list                   # layer widths d_0 .. d_L (d_0 = sum(channels))
+    params: np.ndarray           # uint16 fp16 bits, [D * decoder_stride]
+    tex_to_dec: np.ndarray       # uint32 [T]
+    # queries
+    tex_id: np.ndarray           # uint32 [N]
+    uv: np.ndarray               # float32 [N, 2]
+    mip: Optional[np.ndarray]    # float32 [N] or None (=> 0)
+    screen: Optional[tuple] = None  # (width, height, samples per pixel)
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def n(self) -> int:
+        return int(self.tex_id.shape[0])
+
+    @property
+    def n_levels(self) -> int:
+        return len(self.res)
+
+    @property
+    def n_layers(self) -> int:
+        return len(self.dims) - 1
+
+    @property
+    def out_dim(self) -> int:
+        return int(self.dims[-1])
+
+    @property
+    def texture_stride(self) -> int:
+        return texture_stride(self.res, self.channels)
+
+    @property
+    def decoder_stride(self) -> int:
+        return decoder_stride(self.dims)
+
+    def flops_per_query(self) -> int:
+        """Multiply-adds x 2 of the MLP, unpadded."""
+        return int(sum(2 * a * b for a, b in zip(self.dims[:-1], self.dims[1:])))
+
+    def with_decoders(self, n_decoders: int, tex_to_dec: np.ndarray, seed: int = 0,
+                      name: Optional[str] = None) -> "Workload":
+        """Same grids and queries, a different decoder set and map."""
+        params = draw_decoders(seed, n_decoders, self.dims)
+        return Workload(name or f"{self.name}_d{n_decoders}", self.n_textures, list(self.res),
+                        list(self.channels), self.latents, n_decoders, list(self.dims), params,
+                        np.ascontiguousarray(tex_to_dec, dtype=np.uint32), self.tex_id, self.uv,
+                        self.mip, self.screen, dict(self.meta))
+
+
+def texture_stride(res, channels) -> int:
+    return int(sum(int(r) * int(r) * int(c) for r, c in zip(res, channels)))
+
+
+def decoder_stride(dims) -> int:
+    return int(sum(int(b) * int(a) + int(b) for a, b in zip(dims[:-1], dims[1:])))
+
+
+def level_offsets(res, channels) -> list:
+    """Offset (in fp16 elements) of each level inside one texture's block."""
+    offs, acc = [], 0
+    for r, c in zip(res, channels):
+        offs.append(acc)
+        acc += int(r) * int(r) * int(c)
+    return offs
+
+
+def fp16_bits(a: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float32).astype(np.float16).view(np.uint16))
+
+
+def bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(np.float32)
+
+
+# ----------------------------------------------------------------------------- drawing
+
+
+def draw_latents(seed: int, n_textures: int, res, channels) -> np.ndarray:
+    rng = _rng(seed, _STREAM_LATENTS)
+    total = n_textures * texture_stride(res, channels)
+    out = np.empty(total, dtype=np.uint16)
+    chunk = 1 << 26
+    for s in range(0, total, chunk):
+        e = min(total, s + chunk)
+        out[s:e] = rng.standard_normal(e - s, dtype=np.float32).astype(np.float16).view(np.uint16)
+    return out
+
+
+def draw_decoders(seed: int, n_decoders: int, dims) -> np.ndarray:
+    """Per decoder, contiguous: W0[d1][d0], b0[d1], W1[d2][d1], b1[d2], ...
+
+    All weights are drawn first (decoder-major, layer-major), then all biases.
+    """
+    rng = _rng(seed, _STREAM_DECODERS)
+    ws = []
+    for _ in range(n_decoders):
+        per = []
+        for a, b in zip(dims[:-1], dims[1:]):
+            bound = np.sqrt(6.0 / a)
+            per.append(rng.uniform(-bound, bound, size=(b, a)))
+        ws.append(per)
+    bs = [[rng.uniform(-0.1, 0.1, size=(b,)) for b in dims[1:]] for _ in range(n_decoders)]
+    blob = []
+    for d in range(n_decoders):
+        for w, bb in zip(ws[d], bs[d]):
+            blob.append(w.ravel())
+            blob.append(bb)
+    return fp16_bits(np.concatenate(blob))
+
+
+def zipf_sizes(total: int, parts: int, s: float) -> np.ndarray:
+    """Largest-remainder apportionment of `total` items with weights k^-s."""
+    w = np.arange(1, parts + 1, dtype=np.float64) ** (-s)
+    q = total * w / w.sum()
+    f = np.floor(q).astype(np.int64)
+    rem = total - int(f.sum())
+    order = np.argsort(-(q - f), kind="stable")
+    f[order[:rem]] += 1
+    return f
+
+
+def clustered_map(seed: int, n_textures: int, sizes) -> np.ndarray:
+    """Textures, visited in a seeded random order, fill clusters 0, 1, ... by size."""
+    rng = _rng(seed, _STREAM_MAP)
+    order = rng.permutation(n_textures)
+    m = np.empty(n_textures, dtype=np.uint32)
+    pos = 0
+    for d, sz in enumerate(sizes):
+        m[order[pos:pos + sz]] = d
+        pos += sz
+    assert pos == n_textures
+    return m
+
+
+def equal_map(seed: int, n_textures: int, n_decoders: int) -> np.ndarray:
+    rng = _rng(seed, _STREAM_MAP)
+    return (rng.permutation(n_textures) % n_decoders).astype(np.uint32)
+
+
+def _jittered_uv(rng, width, height, spp, base_x, base_y):
+    """Pixel (x, y) sample s -> ((x + U) / W, (y + U) / H); one U per coordinate."""
+    n = base_x.shape[0]
+    jx = rng.random(n)
+    jy = rng.random(n)
+    u = (base_x + jx) / width
+    v = (base_y + jy) / height
+    return u, v
+
+
+def _pixels(width, height, spp):
+    """Row-major pixel coordinates, repeated per sample: q = (y * W + x) * spp + s."""
+    ys, xs = np.divmod(np.arange(width * height, dtype=np.int64), width)
+    if spp > 1:
+        xs = np.repeat(xs, spp)
+        ys = np.repeat(ys, spp)
+    return xs.astype(np.float64), ys.astype(np.float64)
+
+
+def voronoi_regions(rng, width, height, n_sites) -> np.ndarray:
+    """Region index of every pixel centre: nearest of n_sites uniform sites."""
+    from scipy.spatial import cKDTree
+
+    sites = np.stack([rng.uniform(0, width, n_sites), rng.uniform(0, height, n_sites)], 1)
+    ys, xs = np.divmod(np.arange(width * height, dtype=np.int64), width)
+    pts = np.stack([xs + 0.5, ys + 0.5], 1)
+    _, idx = cKDTree(sites).query(pts, k=1)
+    return idx.astype(np.int64)
+
+
+def _to_f32_uv(u, v):
+    uv = np.stack([u, v], 1).astype(np.float32)
+    np.minimum(uv, F32_BELOW_ONE, out=uv)
+    np.maximum(uv, np.float32(0.0), out=uv)
+    return np.ascontiguousarray(uv)
+
+
+# ----------------------------------------------------------------------------- configs
+
+# Full-size parameters of the five workloads.  Each entry is (generator, kwargs).
+CONFIG_NAMES = ("tiny", "single", "divergent", "clustered4k", "wide_trilinear")
+
+
+def tiny(seed: int = 0, n: int = 65536) -> Workload:
+    """4 textures (64^2x8 + 32^2x8), 2 decoders (t % 2), 16->64->64->8, random queries."""
+    res, ch, dims = [64, 32], [8, 8], [16, 64, 64, 8]
+    lat = draw_latents(seed, 4, res, ch)
+    par = draw_decoders(seed, 2, dims)
+    t2d = (np.arange(4) % 2).astype(np.uint32)
+    rng = _rng(seed, _STREAM_QUERIES)
+    tex = rng.integers(0, 4, size=n).astype(np.uint32)
+    uv = np.ascontiguousarray(rng.random((n, 2), dtype=np.float32))
+    return Workload("tiny", 4, res, ch, lat, 2, dims, par, t2d, tex, uv, None, None)
+
+
+def single(seed: int = 0, width: int = 1920, height: int = 1080) -> Workload:
+    """1 texture (512^2x16 + 256^2x16), 1 decoder, 32->64->64->8, screen-coherent uv."""
+    res, ch, dims = [512, 256], [16, 16], [32, 64, 64, 8]
+    lat = draw_latents(seed, 1, res, ch)
+    par = draw_decoders(seed, 1, dims)
+    rng = _rng(seed, _STREAM_QUERIES)
+    xs, ys = _pixels(width, height, 1)
+    u, v = _jittered_uv(rng, width, height, 1, xs, ys)
+    tex = np.zeros(width * height, dtype=np.uint32)
+    return Workload("single", 1, res, ch, lat, 1, dims, par, np.zeros(1, np.uint32), tex,
+                    _to_f32_uv(u, v), None, (width, height, 1))
+
+
+def divergent(seed: int = 0, width: int = 1920, height: int = 1080) -> Workload:
+    """64 textures, one decoder each; texture fixed per 8x8 pixel tile, uniform in [0, 64)."""
+    res, ch, dims = [256, 128], [16, 16], [32, 64, 64, 8]
+    T = 64
+    lat = draw_latents(seed, T, res, ch)
+    par = draw_decoders(seed, T, dims)
+    t2d = np.arange(T, dtype=np.uint32)
+    lay = _rng(seed, _STREAM_LAYOUT)
+    tw, th = (width + 7) // 8, (height + 7) // 8
+    tile_tex = lay.integers(0, T, size=(th, tw)).astype(np.uint32)
+    rng = _rng(seed, _STREAM_QUERIES)
+    xs, ys = _pixels(width, height, 1)
+    u, v = _jittered_uv(rng, width, height, 1, xs, ys)
+    tex = tile_tex[(ys.astype(np.int64) >> 3), (xs.astype(np.int64) >> 3)]
+    return Workload("divergent", T, res, ch, lat, T, dims, par, t2d,
+                    np.ascontiguousarray(tex, dtype=np.uint32), _to_f32_uv(u, v), None,
+                    (width, height, 1))
+
+
+def _voronoi_queries(seed, width, height, spp, n_sites, n_textures, with_mip):
+    lay = _rng(seed, _STREAM_LAYOUT)
+    region = voronoi_regions(lay, width, height, n_sites)
+    region_tex = lay.integers(0, n_textures, size=n_sites)
+    off = lay.random((n_sites, 2))
+    scale = 2.0 ** lay.uniform(-1.0, 2.0, size=n_sites)
+    rng = _rng(seed, _STREAM_QUERIES)
+    xs, ys = _pixels(width, height, spp)
+    reg = np.repeat(region, spp) if spp > 1 else region
+    jx = rng.random(xs.shape[0])
+    jy = rng.random(xs.shape[0])
+    u = np.mod(off[reg, 0] + scale[reg] * (xs + jx) / width, 1.0)
+    v = np.mod(off[reg, 1] + scale[reg] * (ys + jy) / height, 1.0)
+    mip = None
+    if with_mip:
+        mip = np.ascontiguousarray(rng.uniform(0.0, 2.0, size=xs.shape[0]).astype(np.float32))
+    tex = np.ascontiguousarray(region_tex[reg], dtype=np.uint32)
+    return tex, _to_f32_uv(u, v), mip
+
+
+def _scaled_sites(width, height, full=(3840, 2160), sites=2000):
+    return max(4, int(round(sites * (width * height) / (full[0] * full[1]))))
+
+
+def clustered4k(seed: int = 0, width: int = 3840, height: int = 2160,
+                n_decoders: int = 16, n_textures: int = 512) -> Workload:
+    """512 textures, 16 Zipf(1.1)-sized decoder clusters, Voronoi material map.
+
+    ``n_decoders == n_textures`` gives the per-texture-decoder comparison
+    (identity map).
+    """
+    res, ch, dims = [256, 128], [16, 16], [32, 64, 64, 8]
+    T = n_textures
+    lat = draw_latents(seed, T, res, ch)
+    if n_decoders == T:
+        t2d = np.arange(T, dtype=np.uint32)
+    else:
+        t2d = clustered_map(seed, T, zipf_sizes(T, n_decoders, 1.1))
+    par = draw_decoders(seed, n_decoders, dims)
+    n_sites = _scaled_sites(width, height)
+    tex, uv, _ = _voronoi_queries(seed, width, height, 1, n_sites, T, False)
+    return Workload(f"clustered4k_d{n_decoders}", T, res, ch, lat, n_decoders, dims, par, t2d,
+                    tex, uv, None, (width, height, 1), {"voronoi_sites": n_sites})
+
+
+def wide_trilinear(seed: int = 0, width: int = 3840, height: int = 2160, spp: int = 4,
+                   n_decoders: int = 8, n_textures: int = 512) -> Workload:
+    """512 textures with 3-level pyramids, 48->128->128->128->8, 4 spp, mip ~ U[0, 2)."""
+    res, ch, dims = [512, 256, 128], [16, 16, 16], [48, 128, 128, 128, 8]
+    T = n_textures
+    lat = draw_latents(seed, T, res, ch)
+    if n_decoders == T:
+        t2d = np.arange(T, dtype=np.uint32)
+    else:
+        t2d = equal_map(seed, T, n_decoders)
+    par = draw_decoders(seed, n_decoders, dims)
+    n_sites = _scaled_sites(width, height)
+    tex, uv, mip = _voronoi_queries(seed, width, height, spp, n_sites, T, True)
+    return Workload(f"wide_trilinear_d{n_decoders}", T, res, ch, lat, n_decoders, dims, par, t2d,
+                    tex, uv, mip, (width, height, spp), {"voronoi_sites": n_sites})
+
+
+def make(name: str, seed: int = 0, **kw) -> Workload:
+    gens = {"tiny": tiny, "single": single, "divergent": divergent,
+            "clustered4k": clustered4k, "wide_trilinear": wide_trilinear}
+    return gens[name](seed=seed, **kw)
+
+
+def small(name: str, seed: int = 0) -> Workload:
+    """Reduced-screen version of a workload: same structure, oracle-friendly size.
+
+    The screen sizes are chosen to span many 64-query tiles and to leave a
+    ragged tail (N is not a multiple of 64 or 256).
+    """
+    if name == "tiny":
+        return tiny(seed, n=65536 + 37)
+    if name == "single":
+        return single(seed, 333, 121)
+    if name == "divergent":
+        return divergent(seed, 331, 123)
+    # Fewer textures keep the latent pools small; the decoder maps keep their
+    # structure (Zipf-sized clusters, equal clusters, or one decoder per texture).
+    if name == "clustered4k":
+        return clustered4k(seed, 397, 223, n_decoders=16, n_textures=64)
+    if name == "clustered4k_d512":
+        return clustered4k(seed, 397, 223, n_decoders=64, n_textures=64)
+    if name == "wide_trilinear":
+        return wide_trilinear(seed, 161, 97, 4, n_decoders=8, n_textures=16)
+    if name == "wide_trilinear_d512":
+        return wide_trilinear(seed, 161, 97, 4, n_decoders=16, n_textures=16)
+    raise KeyError(name)

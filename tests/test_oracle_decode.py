@@ -1,0 +1,208 @@
+"""Pins of the oracle's decode: latent sampling and the MLP decoder.
+
+Sampling is checked against torch's grid_sample (bilinear, border padding,
+align_corners=False, float64), against the exact value at texel centres and on
+constant grids.  Level blending by mip is checked against grid_sample of the two
+levels blended by hand.  The MLP is checked against a float64 chain of
+torch.nn.functional.linear, and against zero-weight and identity decoders.
+"""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as Fn
+
+from paper_2608_27888_amd import workloads as W
+
+
+def make_workload(res, ch, T, dims, D, n, seed=0, latents=None, params=None, uv=None, mip=None,
+                  tex=None, t2d=None):
+    rng = np.random.default_rng(seed)
+    stride = W.texture_stride(res, ch)
+    if latents is None:
+        latents = W.fp16_bits(rng.standard_normal(T * stride))
+    if params is None:
+        blob = []
+        for _ in range(D):
+            for a, b in zip(dims[:-1], dims[1:]):
+                blob += [rng.uniform(-1, 1, (b, a)).ravel() * np.sqrt(3.0 / a), rng.uniform(-.1, .1, b)]
+        params = W.fp16_bits(np.concatenate(blob))
+    if tex is None:
+        tex = rng.integers(0, T, n).astype(np.uint32)
+    if t2d is None:
+        t2d = (np.arange(T) % D).astype(np.uint32)
+    if uv is None:
+        uv = rng.uniform(-0.2, 1.2, (n, 2)).astype(np.float32)
+    return W.Workload("t", T, list(res), list(ch), np.ascontiguousarray(latents, np.uint16), D,
+                      list(dims), np.ascontiguousarray(params, np.uint16),
+                      np.ascontiguousarray(t2d, np.uint32), np.ascontiguousarray(tex, np.uint32),
+                      np.ascontiguousarray(uv, np.float32),
+                      None if mip is None else np.ascontiguousarray(mip, np.float32))
+
+
+def level_grid(w, t, l):
+    """Level l of texture t as a float64 [C, H, W] tensor."""
+    off = W.level_offsets(w.res, w.channels)[l] + t * w.texture_stride
+    r, c = w.res[l], w.channels[l]
+    a = W.bits_to_f32(w.latents[off:off + r * r * c]).astype(np.float64).reshape(r, r, c)
+    return torch.from_numpy(a).permute(2, 0, 1).contiguous()
+
+
+def grid_sample_level(w, l, tex, uv):
+    out = np.zeros((uv.shape[0], w.channels[l]))
+    for t in np.unique(tex):
+        sel = np.nonzero(tex == t)[0]
+        g = torch.from_numpy(uv[sel].astype(np.float64) * 2.0 - 1.0).view(1, 1, -1, 2)
+        s = Fn.grid_sample(level_grid(w, int(t), l)[None], g, mode="bilinear",
+                           padding_mode="border", align_corners=False)
+        out[sel] = s[0, :, 0, :].T.numpy()
+    return out
+
+
+def test_half_to_double(oracle):
+    vals = np.array([0.0, -0.0, 1.0, -2.5, 65504.0, 6.1035156e-05, 5.9604645e-08, 0.333],
+                    np.float16)
+    for v in vals:
+        assert oracle.half_to_double(int(v.view(np.uint16))) == float(v)
+    assert np.isinf(oracle.half_to_double(0x7C00))
+    every = np.arange(0, 0x7C00, 97, dtype=np.uint16)
+    got = np.array([oracle.half_to_double(int(b)) for b in every])
+    assert np.array_equal(got, every.view(np.float16).astype(np.float64))
+
+
+@pytest.mark.parametrize("res,ch", [([16, 8], [8, 8]), ([13, 7, 4], [16, 16, 16]), ([32], [4])])
+def test_features_match_grid_sample(oracle, res, ch):
+    w = make_workload(res, ch, T=3, dims=[sum(ch), 8], D=1, n=3000, seed=1)
+    f = oracle.features(w)
+    pos = 0
+    for l in range(len(res)):
+        ref = grid_sample_level(w, l, w.tex_id, w.uv)
+        np.testing.assert_allclose(f[:, pos:pos + ch[l]], ref, rtol=0, atol=1e-12)
+        pos += ch[l]
+
+
+def test_texel_centres_return_stored_latent(oracle):
+    res, ch = [64, 32], [16, 16]
+    rng = np.random.default_rng(2)
+    n = 2000
+    for l in range(2):
+        ix, iy = rng.integers(0, res[l], n), rng.integers(0, res[l], n)
+        uv = np.stack([(ix + 0.5) / res[l], (iy + 0.5) / res[l]], 1).astype(np.float32)
+        w = make_workload(res, ch, T=5, dims=[32, 8], D=1, n=n, seed=3, uv=uv)
+        f = oracle.features(w)[:, 16 * l:16 * l + 16]
+        off = W.level_offsets(res, ch)[l]
+        idx = ((w.tex_id.astype(np.int64) * w.texture_stride + off
+                + (iy * res[l] + ix) * 16)[:, None] + np.arange(16))
+        stored = W.bits_to_f32(w.latents[idx]).astype(np.float64)
+        assert np.array_equal(f, stored)  # exact, not approximate
+
+
+def test_constant_latents_give_constant_output(oracle):
+    res, ch, dims = [32, 16], [8, 8], [16, 64, 64, 8]
+    c = np.float16(0.7109375)
+    lat = np.full(2 * W.texture_stride(res, ch), c.view(np.uint16), np.uint16)
+    w = make_workload(res, ch, T=2, dims=dims, D=1, n=500, seed=4, latents=lat,
+                      uv=np.random.default_rng(0).uniform(-3, 4, (500, 2)).astype(np.float32))
+    assert np.all(oracle.features(w) == float(c))
+    y = oracle.decode(w)
+    assert np.all(y == y[0])
+    # the constant output is the MLP applied to the constant vector, in float64 numpy
+    p = W.bits_to_f32(w.params).astype(np.float64)
+    h, o = np.full(16, float(c)), 0
+    for i, (a, b) in enumerate(zip(dims[:-1], dims[1:])):
+        Wm = p[o:o + a * b].reshape(b, a); o += a * b
+        bb = p[o:o + b]; o += b
+        z = Wm @ h + bb
+        h = np.maximum(z, 0) if i < len(dims) - 2 else 1 / (1 + np.exp(-z))
+    np.testing.assert_allclose(y[0], h, rtol=0, atol=1e-14)
+
+
+@pytest.mark.parametrize("mipval", [0.0, 1.0, 2.0, 0.25, 1.5, 1.999, 3.7, -1.0])
+def test_mip_blending(oracle, mipval):
+    res, ch = [32, 16, 8], [4, 4, 4]
+    n = 800
+    w = make_workload(res, ch, T=2, dims=[12, 8], D=1, n=n, seed=5, mip=np.full(n, mipval))
+    f = oracle.features(w)
+    L = 3
+    m = min(max(float(np.float32(mipval)), 0.0), L - 1)  # the query carries an f32 mip
+    for l in range(L):
+        lod = max(l, m)
+        k0 = int(np.floor(lod)); k1 = min(k0 + 1, L - 1); t = lod - k0
+        a = grid_sample_level(w, k0, w.tex_id, w.uv)
+        b = grid_sample_level(w, k1, w.tex_id, w.uv)
+        ref = a + t * (b - a)
+        np.testing.assert_allclose(f[:, 4 * l:4 * l + 4], ref, rtol=0, atol=1e-12)
+
+
+def test_mip_zero_equals_no_mip(oracle):
+    w = make_workload([32, 16], [8, 8], T=2, dims=[16, 8], D=1, n=600, seed=6,
+                      mip=np.zeros(600))
+    f_mip = oracle.features(w)
+    w.mip = None
+    assert np.array_equal(f_mip, oracle.features(w))
+
+
+@pytest.mark.parametrize("dims", [[16, 64, 64, 8], [32, 64, 64, 8], [48, 128, 128, 128, 8],
+                                  [16, 5, 3]])
+def test_mlp_matches_linear_chain(oracle, dims):
+    F = dims[0]
+    res, ch = ([16, 8], [F // 2, F // 2]) if F % 2 == 0 else ([16], [F])
+    if F == 48:
+        res, ch = [16, 8, 4], [16, 16, 16]
+    w = make_workload(res, ch, T=6, dims=dims, D=3, n=1500, seed=7)
+    x = torch.from_numpy(oracle.features(w))
+    y = oracle.decode(w)
+    p = W.bits_to_f32(w.params).astype(np.float64)
+    stride = W.decoder_stride(dims)
+    dec = w.tex_to_dec[w.tex_id]
+    ref = np.zeros_like(y)
+    for d in range(w.n_decoders):
+        o = d * stride
+        h = x[dec == d]
+        for i, (a, b) in enumerate(zip(dims[:-1], dims[1:])):
+            Wm = torch.from_numpy(p[o:o + a * b].reshape(b, a)); o += a * b
+            bb = torch.from_numpy(p[o:o + b]); o += b
+            z = Fn.linear(h, Wm, bb)
+            h = torch.relu(z) if i < len(dims) - 2 else torch.sigmoid(z)
+        ref[dec == d] = h.numpy()
+    np.testing.assert_allclose(y, ref, rtol=0, atol=1e-13)
+    assert np.all((y > 0) & (y < 1))
+
+
+def test_zero_weights_give_sigmoid_of_bias(oracle):
+    dims = [16, 64, 64, 8]
+    w = make_workload([16, 8], [8, 8], T=2, dims=dims, D=1, n=300, seed=8)
+    p = W.bits_to_f32(w.params).astype(np.float64)
+    o = 0
+    for a, b in zip(dims[:-1], dims[1:]):
+        p[o:o + a * b] = 0.0; o += a * b
+        last_b = p[o:o + b].copy(); o += b
+    w.params = W.fp16_bits(p)
+    y = oracle.decode(w)
+    np.testing.assert_allclose(y, np.broadcast_to(1.0 / (1.0 + np.exp(-last_b)), y.shape),
+                               rtol=4e-16, atol=0)
+    assert np.all(y == y[0])
+
+
+def test_identity_decoder_gives_sigmoid_of_features(oracle):
+    dims = [8, 8]
+    p = np.concatenate([np.eye(8).ravel(), np.zeros(8)])
+    w = make_workload([16], [8], T=2, dims=dims, D=1, n=400, seed=9, params=W.fp16_bits(p))
+    x = oracle.features(w)
+    # equal up to the last-bit differences between libm's and numpy's exp
+    np.testing.assert_allclose(oracle.decode(w), 1.0 / (1.0 + np.exp(-x)), rtol=4e-16, atol=0)
+
+
+def test_invalid_queries_leave_rows_untouched(oracle):
+    w = make_workload([16, 8], [8, 8], T=4, dims=[16, 32, 8], D=2, n=200, seed=10)
+    w.tex_id[::7] = 4                      # past the last texture
+    w.tex_to_dec = np.array([0, 1, 5, 1], np.uint32)  # texture 2 maps past the last decoder
+    y = oracle.decode(w)
+    bad = (w.tex_id >= 4) | np.isin(w.tex_id, [2])
+    assert np.all(np.isnan(y[bad])) and not np.any(np.isnan(y[~bad]))
+
+
+def test_subset_matches_full(oracle):
+    w = make_workload([16, 8], [8, 8], T=4, dims=[16, 32, 8], D=2, n=500, seed=12)
+    full = oracle.decode(w)
+    sub = np.array([499, 0, 17, 17, 250])
+    assert np.array_equal(oracle.decode(w, subset=sub), full[sub])

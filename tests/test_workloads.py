@@ -1,0 +1,40 @@
+"""The seeded input recipes have the structure they claim."""
+import numpy as np
+
+from paper_2608_27888_amd import workloads as W
+
+
+def test_zipf_cluster_sizes():
+    s = W.zipf_sizes(512, 16, 1.1)
+    assert s.tolist() == [169, 79, 50, 37, 29, 24, 20, 17, 15, 13, 12, 11, 10, 9, 9, 8]
+    m = W.clustered_map(0, 512, s)
+    assert np.array_equal(np.bincount(m, minlength=16), s)
+
+
+def test_small_workloads_structure():
+    t = W.small("tiny")
+    assert t.tex_to_dec.tolist() == [0, 1, 0, 1] and t.n % 64 != 0
+    d = W.small("divergent")
+    w, h, _ = d.screen
+    tex = d.tex_id.reshape(h, w)
+    for y in range(0, h, 8):
+        for x in range(0, w, 8):
+            blk = tex[y:y + 8, x:x + 8]
+            assert np.all(blk == blk[0, 0])
+    for name in ("single", "divergent", "clustered4k", "wide_trilinear"):
+        wl = W.small(name)
+        assert wl.uv.dtype == np.float32 and np.all(wl.uv >= 0) and np.all(wl.uv < 1)
+        assert wl.latents.size == wl.n_textures * wl.texture_stride
+        assert wl.params.size == wl.n_decoders * wl.decoder_stride
+        assert wl.dims[0] == sum(wl.channels)
+        assert np.all(wl.tex_id < wl.n_textures) and np.all(wl.tex_to_dec < wl.n_decoders)
+    wt = W.small("wide_trilinear")
+    assert wt.mip is not None and np.all((wt.mip >= 0) & (wt.mip < 2))
+    assert wt.n == 161 * 97 * 4 and np.bincount(wt.tex_to_dec).tolist() == [2] * 8
+
+
+def test_reproducible():
+    a, b = W.small("clustered4k", seed=3), W.small("clustered4k", seed=3)
+    assert np.array_equal(a.uv, b.uv) and np.array_equal(a.latents, b.latents)
+    c = W.small("clustered4k_d512", seed=3)  # same queries and grids, other decoders
+    assert np.array_equal(a.tex_id, c.tex_id) and np.array_equal(a.latents, c.latents)
