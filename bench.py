@@ -1,0 +1,261 @@
+"""Throughput of neural texture decode with per-wave decoder binning on one MI355X.
+
+One step = one pass of the hot path over one frame of queries, inputs resident
+in HBM: ntc_build_bins (histogram, scan, stable scatter) followed by the binned
+ntc_decode (gather + MFMA MLP + sigmoid + store).  Default workload: the 4K
+clustered frame (3840x2160 queries, 512 textures, 16 Zipf-sized decoder
+clusters, Voronoi material map).
+
+Prints one JSON line.  Besides the headline it reports the decode kernel's
+roofline position (HIP events over the timed region), the CPU oracle timed on a
+bounded sample of the same frame, mean decoders per wave in stream and binned
+order, and (unless --no-compare) the divergent-vs-clustered 2x2: {512
+per-texture decoders, 16 clusters} x {stream order, binned}.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E, GB/s
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 MFMA, TFLOP/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="clustered4k",
+                   choices=["clustered4k", "single", "divergent", "wide_trilinear"])
+    p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--no-compare", action="store_true",
+                   help="skip the stream/binned x 16/512-decoder comparison runs")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample", type=int, default=1 << 22,
+                   help="queries of the frame the CPU oracle decodes")
+    return p.parse_args()
+
+
+def unique_latent_bytes(w) -> int:
+    """Bytes of distinct latent texels a frame touches (bilinear taps, mip 0 only)."""
+    if w.mip is not None:
+        return 0  # not counted for blended levels
+    total = 0
+    u = w.uv[:, 0].astype(np.float32)
+    v = w.uv[:, 1].astype(np.float32)
+    tex = w.tex_id.astype(np.int64)
+    for l, (r, c) in enumerate(zip(w.res, w.channels)):
+        x0 = np.floor(u * np.float32(r) - np.float32(0.5)).astype(np.int64)
+        y0 = np.floor(v * np.float32(r) - np.float32(0.5)).astype(np.int64)
+        keys = []
+        for dx in (0, 1):
+            for dy in (0, 1):
+                xx = np.clip(x0 + dx, 0, r - 1)
+                yy = np.clip(y0 + dy, 0, r - 1)
+                keys.append((tex * r + yy) * r + xx)
+        total += np.unique(np.concatenate(keys)).size * c * 2
+    return int(total)
+
+
+def timed(fn, steps, warmup, torch):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the decode path shards by screen slabs with no exchange; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_27888_amd import ntc
+    from paper_2608_27888_amd import workloads as W
+    from paper_2608_27888_amd.report import divergence_metric, paper_speedup_percent
+
+    dev = torch.device("cuda:0")
+    ntc.lib()
+    t0 = time.time()
+    w = W.make(args.workload, seed=args.seed)
+    log(f"[bench] workload {w.name}: n={w.n} T={w.n_textures} D={w.n_decoders} dims={w.dims} "
+        f"levels={w.res}x{w.channels} ({time.time() - t0:.1f} s to draw)")
+    model, q = ntc.upload(w, dev)
+    n = w.n
+    bins = ntc.alloc_bins(n, w.n_decoders, 64, dev)
+    out = torch.empty((n, w.out_dim), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    # ---------------------------------------------------------------- headline
+    ev = []
+
+    def step():
+        ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders, bins=bins, stream=stream)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        ntc.decode(model, q, bins, out=out, stream=stream)
+        e1.record(stream)
+        ev.append((e0, e1))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev.clear()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms_step = wall * 1e3 / args.steps
+    decode_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    log(f"[bench] step {ms_step:.4f} ms, decode kernel {decode_ms:.4f} ms")
+    assert ntc.device_error(bins) == 0
+
+    # bins alone, for the breakdown
+    bins_ms = timed(lambda: ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders, bins=bins,
+                                           stream=stream), args.steps, args.warmup, torch) * 1e3
+
+    # ---------------------------------------------------------------- roofline
+    flops_q = w.flops_per_query()
+    stream_bytes_q = 4 + 4 + 8 + 4 * w.out_dim + (4 if w.mip is not None else 0)
+    lat_bytes = unique_latent_bytes(w)
+    used = np.unique(w.tex_to_dec[w.tex_id])
+    param_bytes = int(used.size * w.decoder_stride * 2)
+    decode_bytes = n * stream_bytes_q + lat_bytes + param_bytes
+    decode_flops = n * flops_q
+    t_hbm = decode_bytes / (HBM_PEAK_GBS * 1e9)
+    t_mfma = decode_flops / (MFMA_F16_PEAK_TFLOPS * 1e12)
+    dsec = decode_ms * 1e-3
+    if t_hbm >= t_mfma:
+        roof = {"bound": "hbm", "achieved": round(decode_bytes / dsec / 1e9, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": round(decode_flops / dsec / 1e12, 1),
+                "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = None
+    roof["kernel"] = "decode_binned"
+    roof["algorithmic_bytes_per_launch"] = int(decode_bytes)
+    roof["algorithmic_flops_per_launch"] = int(decode_flops)
+    # end-to-end: binning adds 12 B per query (read ids twice, write the permutation)
+    e2e_bytes = decode_bytes + 12 * n
+    e2e_roof_ms = max(e2e_bytes / (HBM_PEAK_GBS * 1e9), t_mfma) * 1e3
+
+    # ---------------------------------------------------------------- divergence
+    per_s, tot_s = ntc.divergence_stats(q.tex_id, model.tex_to_dec, w.n_decoders)
+    P = int(bins.bin_offset[-1].item())
+    per_b, tot_b = ntc.divergence_stats(q.tex_id, model.tex_to_dec, w.n_decoders,
+                                        order=bins.perm[:P])
+    tot_s, tot_b = tot_s.cpu().tolist(), tot_b.cpu().tolist()
+
+    result = {
+        "metric": "decoded texels/sec (Gtexel/s) on 1 MI355X; MFMA util %; mean decoders/wave",
+        "value": round(n / (ms_step * 1e-3) / 1e9, 3),
+        "unit": "Gtexel/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "queries": n, "screen": list(w.screen or []),
+                   "textures": w.n_textures, "decoders": w.n_decoders, "mlp": list(w.dims),
+                   "latent_levels": [[r, r, c] for r, c in zip(w.res, w.channels)],
+                   "parallelism": "single GPU", "step": "build_bins + binned decode"},
+        "decode_only_gtexel_s": round(n / dsec / 1e9, 3),
+        "decode_ms": round(decode_ms, 5),
+        "build_bins_ms": round(bins_ms, 5),
+        "mfma_util_pct": round(100.0 * decode_flops / dsec / (MFMA_F16_PEAK_TFLOPS * 1e12), 2),
+        "roofline": roof,
+        "end_to_end_roofline_frac": round(e2e_roof_ms / ms_step, 4),
+        "mean_decoders_per_wave": {"stream": round(tot_s[1] / max(tot_s[0], 1), 4),
+                                   "binned": round(tot_b[1] / max(tot_b[0], 1), 4),
+                                   "divergence_metric_stream": round(divergence_metric(tot_s), 4),
+                                   "divergence_metric_binned": round(divergence_metric(tot_b), 4)},
+    }
+
+    # ---------------------------------------------------------------- 2x2 comparison
+    if not args.no_compare and w.name.startswith(("clustered4k", "wide_trilinear")):
+        T = w.n_textures
+        w512 = w.with_decoders(T, np.arange(T, dtype=np.uint32), seed=args.seed)
+        m512, _ = ntc.upload(w512, dev)
+        bins512 = ntc.alloc_bins(n, T, 64, dev)
+        reps = max(3, args.steps // 4)
+
+        def run(m, D, b, binned):
+            def f():
+                if binned:
+                    ntc.build_bins(q.tex_id, m.tex_to_dec, D, bins=b, stream=stream)
+                    ntc.decode(m, q, b, out=out, stream=stream)
+                else:
+                    ntc.decode(m, q, None, out=out, stream=stream)
+            return timed(f, reps, 2, torch) * 1e3
+
+        t = {"d16_binned": ms_step,
+             "d16_stream": run(model, w.n_decoders, bins, False),
+             f"d{T}_binned": run(m512, T, bins512, True),
+             f"d{T}_stream": run(m512, T, bins512, False)}
+        _, ts512 = ntc.divergence_stats(q.tex_id, m512.tex_to_dec, T)
+        ts512 = ts512.cpu().tolist()
+        result["compare_ms"] = {k: round(v, 4) for k, v in t.items()}
+        result["compare_decoders_per_wave_stream"] = {
+            f"d{w.n_decoders}": result["mean_decoders_per_wave"]["stream"],
+            f"d{T}": round(ts512[1] / max(ts512[0], 1), 4)}
+        result["speedup_divergent_vs_clustered_binned"] = round(t[f"d{T}_stream"] / ms_step, 3)
+        result["speedup_paper_percent_form"] = round(
+            paper_speedup_percent([ms_step], [t[f"d{T}_stream"]]), 2)
+        result["paper_context"] = ("paper: up to 8.48x (848.49 %) shared vs non-shared WMMA, "
+                                   "10 decoders per wave, RX 9070 XT at 1.6 GHz")
+        log(f"[bench] compare {result['compare_ms']}")
+
+    # ---------------------------------------------------------------- CPU oracle
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+
+        threads = O.default_threads()
+        k = max(1, n // args.cpu_sample)
+        sub = np.arange(0, n, k, dtype=np.int64)[: args.cpu_sample]
+        tb = time.perf_counter()
+        O.build_bins(w.tex_id, w.tex_to_dec, w.n_decoders, 64)
+        tb = time.perf_counter() - tb
+        td = time.perf_counter()
+        O.decode(w, subset=sub, threads=threads)
+        td = time.perf_counter() - td
+        t_sample = td + tb * sub.size / n
+        result["cpu_baseline"] = {
+            "value": round(sub.size / t_sample / 1e9, 6), "unit": "Gtexel/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"every {k}-th query of the frame ({sub.size} queries) decoded in float64, "
+                      f"plus binning of the whole frame scaled to the sample; "
+                      f"{t_sample:.2f} s"}
+        log(f"[bench] cpu oracle {result['cpu_baseline']}")
+
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,192 @@
+/*
+ * ntc.h -- C ABI of libntc: neural texture decode with per-wave decoder binning
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * What is computed (paper: "Thread-Efficient Decoding for Neural Texture
+ * Compression"):
+ *   - each texture i owns a multi-resolution latent grid (its "encoder" output,
+ *     Sec. 1) and uses decoder c(i) (Alg. "Overall texture processing
+ *     pipeline", Stage 2, the texture -> group map);
+ *   - a texel query (texture, uv, mip) samples the latent grid, concatenates
+ *     the per-level samples and runs the texture's MLP decoder (Sec. 1 and the
+ *     setup paragraph of Sec. 4);
+ *   - a wave that decodes queries of k distinct decoders runs k serial tensor
+ *     passes (Sec. 1 and Sec. 4.4); ntc_build_bins groups queries by decoder id
+ *     so that every 64-lane wave of ntc_decode runs exactly one decoder;
+ *   - ntc_divergence_stats counts distinct decoders per wave-sized block, the
+ *     divergence map of Sec. 2, and the totals behind the metric of
+ *     Eq. (normalized_ones_metric).
+ *
+ * Conventions for every entry point:
+ *   - Pointers are DEVICE pointers unless marked (host).  The caller owns every
+ *     buffer; the library never allocates device memory and keeps no state
+ *     between calls.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *     device work is enqueued on it and the call returns without waiting,
+ *     except ntc_get_device_error, which synchronises the stream.
+ *   - Calls on different streams are independent; two calls that share an
+ *     output or workspace buffer must be ordered by the caller.
+ *   - Arguments are validated on the host before anything is enqueued; on an
+ *     error nothing is enqueued and a negative ntc_status is returned.
+ */
+#ifndef NTC_H
+#define NTC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  NTC_OK = 0,
+  NTC_ERR_ARG = -1,         /* NULL pointer, negative or too large size, bad alignment */
+  NTC_ERR_UNSUPPORTED = -2, /* a shape the kernels are not built for */
+  NTC_ERR_CAPACITY = -3,    /* an output or workspace buffer is too small */
+  NTC_ERR_HIP = -4,         /* a HIP runtime call failed */
+  NTC_ERR_INDEX = -5        /* device-side: a query named a texture or decoder out of range */
+} ntc_status;
+
+#define NTC_PAD 0xFFFFFFFFu /* padding entry of a bin in `perm` */
+#define NTC_MAX_LEVELS 4
+#define NTC_MAX_LAYERS 8
+#define NTC_MAX_DECODERS 4096 /* binning keeps one counter per decoder in LDS */
+#define NTC_MAX_ALIGN 4096
+
+/*
+ * Latent grids, one block per texture, all textures alike.  Level l is a
+ * res[l] x res[l] grid of channels[l] fp16 values per texel, stored [y][x][c]
+ * (channel-last).  Texture t starts at latents + t * S, S = sum_l res[l]^2 *
+ * channels[l]; inside it the levels follow one another, finest first.
+ * Sampling (Sec. 1 "latent pyramids or grids"): bilinear, texel centres at
+ * ((i + 1/2) / res, (j + 1/2) / res), clamp-to-edge addressing.
+ */
+typedef struct {
+  int32_t n_textures;
+  int32_t n_levels;                  /* 1 .. NTC_MAX_LEVELS */
+  int32_t res[NTC_MAX_LEVELS];       /* (host values) */
+  int32_t channels[NTC_MAX_LEVELS];  /* (host values) */
+  const uint16_t *latents;           /* fp16 bit patterns */
+} ntc_grids;
+
+/*
+ * MLP decoders (Sec. 4 setup: an MLP of a few fully connected layers).  Layer
+ * i maps dims[i] -> dims[i+1]: z = W_i h + b_i, W_i row-major [dims[i+1]][dims[i]].
+ * Hidden layers apply ReLU, the last layer the logistic sigmoid, so decoded
+ * channels lie in [0, 1].  Decoder d occupies params + d * P with
+ * P = sum_i dims[i+1] * (dims[i] + 1) fp16 values laid out W_0, b_0, W_1, b_1, ...
+ */
+typedef struct {
+  int32_t n_decoders;
+  int32_t n_layers;                  /* 1 .. NTC_MAX_LAYERS */
+  int32_t dims[NTC_MAX_LAYERS + 1];  /* (host values); dims[0] = sum of grid channels */
+  const uint16_t *params;            /* fp16 bit patterns */
+} ntc_decoders;
+
+/*
+ * Query stream, one entry per texel request in issue order (row-major pixels,
+ * samples innermost).  uv is [n][2] float; any finite uv is valid (taps clamp
+ * to the edge).  mip may be NULL (all zero).  With a mip, slot l of the
+ * feature vector samples the pyramid at level of detail max(l, mip), mip
+ * clamped to [0, n_levels-1], blending the two levels around it linearly; all
+ * levels must then have the same channel count.
+ */
+typedef struct {
+  const uint32_t *tex_id;  /* [n] */
+  const float *uv;         /* [n][2] */
+  const float *mip;        /* [n] or NULL */
+  int64_t n;               /* 0 .. 2^32 - 2 */
+} ntc_queries;
+
+/* (host) Bytes of device workspace ntc_build_bins needs for n queries and
+ * n_decoders bins; 0 when the arguments are out of range. */
+size_t ntc_bins_workspace_bytes(int64_t n, int32_t n_decoders);
+
+/* (host) Entries `perm` must hold: n + n_decoders * (align - 1), the largest
+ * padded total; -1 when the arguments are out of range. */
+int64_t ntc_bins_capacity(int64_t n, int32_t n_decoders, int32_t align);
+
+/*
+ * Bin queries by decoder id: a stable counting sort.  With d(q) =
+ * tex_to_dec[tex_id[q]]:
+ *   bin_count[d]  = |{q : d(q) = d}|                          (u32 [n_decoders])
+ *   bin_offset[0] = 0, bin_offset[d+1] = bin_offset[d] + roundup(bin_count[d], align)
+ *                                                             (u32 [n_decoders + 1])
+ *   perm[bin_offset[d] + r] = the r-th query of decoder d in ascending q order;
+ *   slots [bin_offset[d] + bin_count[d], bin_offset[d+1]) hold NTC_PAD; entries
+ *   at and past bin_offset[n_decoders] are left untouched.
+ * The result is unique, so it is reproducible bit for bit.  Queries with
+ * tex_id >= n_textures or d(q) >= n_decoders are left out of every bin and
+ * counted; read the count with ntc_get_device_error.
+ * align: power of two in [1, NTC_MAX_ALIGN]; 64 (one wave) for ntc_decode.
+ * perm_capacity >= ntc_bins_capacity(n, n_decoders, align) (NTC_ERR_CAPACITY).
+ * workspace: device buffer of >= ntc_bins_workspace_bytes(n, n_decoders) bytes,
+ * owned by the caller, contents need not be initialised; it holds the
+ * invalid-query count until the next call that uses it.
+ * n = 0 is valid: bin_count and bin_offset become all zero.
+ */
+int ntc_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
+                   int32_t n_textures, int32_t n_decoders, int32_t align,
+                   uint32_t *bin_count, uint32_t *bin_offset, uint32_t *perm,
+                   int64_t perm_capacity, void *workspace, size_t workspace_bytes,
+                   void *stream);
+
+/*
+ * (synchronises `stream`) Number of queries the last ntc_build_bins on this
+ * workspace left out because of an out-of-range texture or decoder id; writes it
+ * to *n_invalid (host, may be NULL).  Returns NTC_OK when it is zero,
+ * NTC_ERR_INDEX otherwise.
+ */
+int ntc_get_device_error(const void *workspace, uint64_t *n_invalid, void *stream);
+
+/*
+ * Decode every query: out[q][c] = MLP_{d(q)}(features(q))[c], float32,
+ * [n][dims[n_layers]] row-major, rows in original query order.
+ *   Binned mode (bin_offset != NULL): queries are taken from `perm` in tiles of
+ *   64 consecutive slots, each tile belonging to one bin (align must be a
+ *   multiple of 64 and equal to the align given to ntc_build_bins); the tile's
+ *   decoder is its bin's, and tex_to_dec is not read.  NTC_PAD slots and slots
+ *   holding q >= n are skipped.  perm_capacity must be the capacity passed to
+ *   ntc_build_bins.
+ *   Stream mode (bin_offset == NULL): tiles are 64 consecutive queries; a wave
+ *   whose tile holds k distinct decoders runs the MLP k times (the divergent
+ *   execution of Sec. 1 and Sec. 4.4); perm is ignored.
+ * Rows of queries with tex_id >= n_textures (or, in stream mode, a decoder id
+ * >= n_decoders) are left untouched.  A query's result depends only on that
+ * query, so both modes give identical bits.
+ * Supported shapes (else NTC_ERR_UNSUPPORTED): (n_levels, channels per level)
+ * in {(2, 8), (2, 16), (3, 16)}, the same channel count on every level and
+ * dims[0] = their sum; 2 .. 5 layers whose hidden widths are all equal, 64 or
+ * 128; dims[n_layers] in 1 .. 16; level resolutions in 1 .. 16384; latents of
+ * one texture < 2^31 values.  Other malformed shapes give NTC_ERR_ARG.
+ */
+int ntc_decode(const ntc_grids *grids, const ntc_decoders *decoders,
+               const uint32_t *tex_to_dec, const ntc_queries *queries,
+               const uint32_t *bin_offset, const uint32_t *perm, int64_t perm_capacity,
+               int32_t align, float *out, void *stream);
+
+/*
+ * Divergence per wave-sized block (Sec. 2): for window w = entries
+ * [w * wave, min(len, (w+1) * wave)) of an order, per_wave_distinct[w] = number
+ * of distinct decoder ids d(q) over the window's entries q = order[i] (order ==
+ * NULL: q = i).  Entries with q >= n (NTC_PAD included), tex_id[q] >= n_textures
+ * or d(q) >= n_decoders are skipped.  totals (u64 [4]) = {windows with at least
+ * one entry kept, sum of per_wave_distinct, windows with more than one decoder,
+ * largest per_wave_distinct}.  The metric of Eq. (normalized_ones_metric) over
+ * the kept windows is totals[1] / totals[0] - 1.  Pass an identity tex_to_dec
+ * to count distinct textures instead.  wave: 1 .. 64.
+ * per_wave_distinct: u32 [ceil(len / wave)].
+ */
+int ntc_divergence_stats(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
+                         int32_t n_textures, int32_t n_decoders, const uint32_t *order,
+                         int64_t len, int32_t wave, uint32_t *per_wave_distinct,
+                         uint64_t *totals, void *stream);
+
+/* (host) Static description of a status code. */
+const char *ntc_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NTC_H */

@@ -1,0 +1,148 @@
+// ntc_api.hip -- the extern "C" entry points of libntc: host-side validation,
+// then the kernel launches of ntc_bins.hip, ntc_decode.hip, ntc_divergence.hip.
+#include "ntc_internal.h"
+
+using namespace ntc;
+
+namespace {
+
+constexpr int64_t kMaxQueries = 0xFFFFFFFELL;  // ids and slots are 32-bit; NTC_PAD reserved
+
+bool pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char *ntc_status_string(int status) {
+  switch (status) {
+    case NTC_OK: return "ok";
+    case NTC_ERR_ARG: return "invalid argument";
+    case NTC_ERR_UNSUPPORTED: return "unsupported shape";
+    case NTC_ERR_CAPACITY: return "buffer too small";
+    case NTC_ERR_HIP: return "HIP runtime error";
+    case NTC_ERR_INDEX: return "texture or decoder id out of range";
+    default: return "unknown status";
+  }
+}
+
+size_t ntc_bins_workspace_bytes(int64_t n, int32_t n_decoders) {
+  if (n < 0 || n > kMaxQueries || n_decoders < 1 || n_decoders > NTC_MAX_DECODERS) return 0;
+  return bins_layout(n, n_decoders).bytes;
+}
+
+int64_t ntc_bins_capacity(int64_t n, int32_t n_decoders, int32_t align) {
+  if (n < 0 || n > kMaxQueries || n_decoders < 1 || n_decoders > NTC_MAX_DECODERS ||
+      !pow2(align) || align > NTC_MAX_ALIGN)
+    return -1;
+  return n + (int64_t)n_decoders * (align - 1);
+}
+
+int ntc_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
+                   int32_t n_textures, int32_t n_decoders, int32_t align,
+                   uint32_t *bin_count, uint32_t *bin_offset, uint32_t *perm,
+                   int64_t perm_capacity, void *workspace, size_t workspace_bytes,
+                   void *stream) {
+  if (n < 0 || n > kMaxQueries || n_textures < 1 || n_decoders < 1 ||
+      n_decoders > NTC_MAX_DECODERS || !pow2(align) || align > NTC_MAX_ALIGN)
+    return NTC_ERR_ARG;
+  if (!tex_to_dec || !bin_count || !bin_offset || !workspace || (n > 0 && (!tex_id || !perm)))
+    return NTC_ERR_ARG;
+  const int64_t cap = ntc_bins_capacity(n, n_decoders, align);
+  if (perm_capacity < cap || cap > kMaxQueries + 1) return NTC_ERR_CAPACITY;
+  if (workspace_bytes < ntc_bins_workspace_bytes(n, n_decoders)) return NTC_ERR_CAPACITY;
+  return launch_build_bins(tex_id, n, tex_to_dec, n_textures, n_decoders, align, bin_count,
+                           bin_offset, perm, workspace, (hipStream_t)stream);
+}
+
+int ntc_get_device_error(const void *workspace, uint64_t *n_invalid, void *stream) {
+  if (!workspace) return NTC_ERR_ARG;
+  return read_invalid_count(workspace, n_invalid, (hipStream_t)stream);
+}
+
+int ntc_decode(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex_to_dec,
+               const ntc_queries *q, const uint32_t *bin_offset, const uint32_t *perm,
+               int64_t perm_capacity, int32_t align, float *out, void *stream) {
+  if (!g || !m || !q) return NTC_ERR_ARG;
+  if (q->n < 0 || q->n > kMaxQueries) return NTC_ERR_ARG;
+  if (g->n_textures < 1 || g->n_levels < 1 || g->n_levels > NTC_MAX_LEVELS) return NTC_ERR_ARG;
+  if (m->n_decoders < 1 || m->n_decoders > NTC_MAX_DECODERS || m->n_layers < 1 ||
+      m->n_layers > NTC_MAX_LAYERS)
+    return NTC_ERR_ARG;
+  const bool binned = bin_offset != nullptr;
+  if (q->n > 0 && (!g->latents || !m->params || !q->tex_id || !q->uv || !out))
+    return NTC_ERR_ARG;
+  if (binned) {
+    if (!perm || align < 64 || !pow2(align) || align > NTC_MAX_ALIGN) return NTC_ERR_ARG;
+    if (perm_capacity < ntc_bins_capacity(q->n, m->n_decoders, align)) return NTC_ERR_CAPACITY;
+  } else if (!tex_to_dec && q->n > 0) {
+    return NTC_ERR_ARG;
+  }
+  // grid shape
+  const int L = g->n_levels;
+  const int ch = g->channels[0];
+  int64_t tex_stride = 0;
+  DecodeArgs a = {};
+  for (int l = 0; l < L; ++l) {
+    const int r = g->res[l];
+    if (r < 1 || r > 16384 || g->channels[l] < 1) return NTC_ERR_ARG;
+    if (g->channels[l] != ch) return NTC_ERR_UNSUPPORTED;
+    a.level_off[l] = (int32_t)tex_stride;
+    a.res[l] = r;
+    a.resf[l] = (float)r;
+    tex_stride += (int64_t)r * r * ch;
+    if (tex_stride >= ((int64_t)1 << 31)) return NTC_ERR_UNSUPPORTED;
+  }
+  // decoder shape: dims[0] = features, equal hidden widths, small output
+  const int F = L * ch;
+  const int nl = m->n_layers;
+  if (m->dims[0] != F) return NTC_ERR_ARG;
+  for (int i = 0; i <= nl; ++i)
+    if (m->dims[i] < 1) return NTC_ERR_ARG;
+  if (nl < 2) return NTC_ERR_UNSUPPORTED;
+  const int hid = m->dims[1];
+  for (int i = 1; i < nl; ++i)
+    if (m->dims[i] != hid) return NTC_ERR_UNSUPPORTED;
+  const int out_dim = m->dims[nl];
+  if (out_dim > 16) return NTC_ERR_UNSUPPORTED;
+  int64_t dec_stride = 0;
+  for (int i = 0; i < nl; ++i) dec_stride += (int64_t)m->dims[i + 1] * (m->dims[i] + 1);
+
+  a.latents = g->latents;
+  a.tex_stride = tex_stride;
+  a.n_textures = g->n_textures;
+  a.params = m->params;
+  a.dec_stride = dec_stride;
+  a.n_decoders = m->n_decoders;
+  a.n_hidden = nl - 2;
+  a.out_dim = out_dim;
+  a.tex_to_dec = tex_to_dec;
+  a.tex_id = q->tex_id;
+  a.uv = q->uv;
+  a.mip = q->mip;
+  a.n = (uint32_t)q->n;
+  a.bin_offset = bin_offset;
+  a.perm = perm;
+  a.perm_capacity = binned ? (uint64_t)perm_capacity : 0;
+  a.max_tiles = binned ? (uint32_t)((ntc_bins_capacity(q->n, m->n_decoders, align) + 63) / 64)
+                       : (uint32_t)((q->n + 63) / 64);
+  a.out = out;
+  if (q->n == 0) return NTC_OK;
+  return launch_decode(a, L, ch, F, hid, (hipStream_t)stream);
+}
+
+int ntc_divergence_stats(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
+                         int32_t n_textures, int32_t n_decoders, const uint32_t *order,
+                         int64_t len, int32_t wave, uint32_t *per_wave_distinct,
+                         uint64_t *totals, void *stream) {
+  if (n < 0 || n > kMaxQueries || len < 0 || n_textures < 1 || n_decoders < 1 || wave < 1 ||
+      wave > 64 || !totals || !tex_to_dec)
+    return NTC_ERR_ARG;
+  if (!order && len > n) return NTC_ERR_ARG;
+  if (order && len > kMaxQueries + 1) return NTC_ERR_ARG;
+  if (len > 0 && (!per_wave_distinct || (n > 0 && !tex_id))) return NTC_ERR_ARG;
+  return launch_divergence(tex_id, n, tex_to_dec, n_textures, n_decoders, order, len, wave,
+                           per_wave_distinct, totals, (hipStream_t)stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,273 @@
+"""Python binding of libntc (ctypes): argument marshalling only.
+
+Every step of the decode path runs in the HIP kernels of ``libntc.so``; this
+module passes device pointers (``tensor.data_ptr()``) and the current HIP
+stream.  PyTorch is used for device memory and streams only.  There is no
+fallback: if the library is missing the import of the binding fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libntc.so")
+
+NTC_OK = 0
+NTC_ERR_ARG = -1
+NTC_ERR_UNSUPPORTED = -2
+NTC_ERR_CAPACITY = -3
+NTC_ERR_HIP = -4
+NTC_ERR_INDEX = -5
+NTC_PAD = 0xFFFFFFFF
+MAX_LEVELS = 4
+MAX_LAYERS = 8
+
+
+class NtcError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {status} ({status_string(status)})")
+        self.status = status
+
+
+class Grids(ctypes.Structure):
+    _fields_ = [("n_textures", ctypes.c_int32), ("n_levels", ctypes.c_int32),
+                ("res", ctypes.c_int32 * MAX_LEVELS), ("channels", ctypes.c_int32 * MAX_LEVELS),
+                ("latents", ctypes.c_void_p)]
+
+
+class Decoders(ctypes.Structure):
+    _fields_ = [("n_decoders", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("dims", ctypes.c_int32 * (MAX_LAYERS + 1)), ("params", ctypes.c_void_p)]
+
+
+class Queries(ctypes.Structure):
+    _fields_ = [("tex_id", ctypes.c_void_p), ("uv", ctypes.c_void_p), ("mip", ctypes.c_void_p),
+                ("n", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2608_27888_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        L.ntc_status_string.argtypes = [ctypes.c_int]
+        L.ntc_status_string.restype = ctypes.c_char_p
+        L.ntc_bins_workspace_bytes.argtypes = [i64, i32]
+        L.ntc_bins_workspace_bytes.restype = sz
+        L.ntc_bins_capacity.argtypes = [i64, i32, i32]
+        L.ntc_bins_capacity.restype = i64
+        L.ntc_build_bins.argtypes = [P, i64, P, i32, i32, i32, P, P, P, i64, P, sz, P]
+        L.ntc_get_device_error.argtypes = [P, P, P]
+        L.ntc_decode.argtypes = [ctypes.POINTER(Grids), ctypes.POINTER(Decoders), P,
+                                 ctypes.POINTER(Queries), P, P, i64, i32, P, P]
+        L.ntc_divergence_stats.argtypes = [P, i64, P, i32, i32, P, i64, i32, P, P, P]
+        for f in ("ntc_build_bins", "ntc_get_device_error", "ntc_decode", "ntc_divergence_stats"):
+            getattr(L, f).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().ntc_status_string(int(status)).decode()
+
+
+def _check(fn: str, status: int):
+    if status != NTC_OK:
+        raise NtcError(fn, status)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("libntc takes device tensors")
+    if not t.is_contiguous():
+        raise ValueError("libntc takes contiguous tensors")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream: Optional[torch.cuda.Stream]):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+# ----------------------------------------------------------------------------- binning
+
+
+def workspace_bytes(n: int, n_decoders: int) -> int:
+    return int(lib().ntc_bins_workspace_bytes(n, n_decoders))
+
+
+def perm_capacity(n: int, n_decoders: int, align: int = 64) -> int:
+    return int(lib().ntc_bins_capacity(n, n_decoders, align))
+
+
+@dataclass
+class Bins:
+    """Outputs of ntc_build_bins (device tensors, uint32 stored as int32)."""
+
+    bin_count: torch.Tensor
+    bin_offset: torch.Tensor
+    perm: torch.Tensor
+    workspace: torch.Tensor
+    align: int
+
+    @property
+    def capacity(self) -> int:
+        return int(self.perm.numel())
+
+
+def alloc_bins(n: int, n_decoders: int, align: int = 64, device="cuda") -> Bins:
+    cap = perm_capacity(n, n_decoders, align)
+    ws = workspace_bytes(n, n_decoders)
+    if cap < 0 or ws == 0:
+        raise NtcError("alloc_bins", NTC_ERR_ARG)
+    return Bins(torch.empty(n_decoders, dtype=torch.int32, device=device),
+                torch.empty(n_decoders + 1, dtype=torch.int32, device=device),
+                torch.empty(max(cap, 1), dtype=torch.int32, device=device),
+                torch.empty(ws, dtype=torch.uint8, device=device), align)
+
+
+def build_bins(tex_id: torch.Tensor, tex_to_dec: torch.Tensor, n_decoders: int, align: int = 64,
+               n_textures: Optional[int] = None, bins: Optional[Bins] = None,
+               stream=None) -> Bins:
+    n = int(tex_id.numel())
+    T = int(tex_to_dec.numel()) if n_textures is None else int(n_textures)
+    if bins is None:
+        bins = alloc_bins(n, n_decoders, align, tex_id.device)
+    _check("ntc_build_bins", lib().ntc_build_bins(
+        _ptr(tex_id), n, _ptr(tex_to_dec), T, n_decoders, align, _ptr(bins.bin_count),
+        _ptr(bins.bin_offset), _ptr(bins.perm), bins.capacity, _ptr(bins.workspace),
+        int(bins.workspace.numel()), _stream(stream)))
+    return bins
+
+
+def device_error(bins: Bins, stream=None) -> int:
+    """Synchronises; returns the number of queries left out of every bin."""
+    v = ctypes.c_uint64(0)
+    st = lib().ntc_get_device_error(_ptr(bins.workspace), ctypes.byref(v), _stream(stream))
+    if st not in (NTC_OK, NTC_ERR_INDEX):
+        raise NtcError("ntc_get_device_error", st)
+    return int(v.value)
+
+
+# ----------------------------------------------------------------------------- decode
+
+
+@dataclass
+class DeviceModel:
+    """Latent grids, decoders and the texture -> decoder map, resident on the device."""
+
+    n_textures: int
+    res: list
+    channels: list
+    latents: torch.Tensor      # int16 view of fp16 bits
+    n_decoders: int
+    dims: list
+    params: torch.Tensor       # int16 view of fp16 bits
+    tex_to_dec: torch.Tensor   # int32 view of uint32
+
+    def grids(self) -> Grids:
+        g = Grids()
+        g.n_textures = self.n_textures
+        g.n_levels = len(self.res)
+        for i, (r, c) in enumerate(zip(self.res, self.channels)):
+            g.res[i] = r
+            g.channels[i] = c
+        g.latents = _ptr(self.latents)
+        return g
+
+    def decoders(self) -> Decoders:
+        d = Decoders()
+        d.n_decoders = self.n_decoders
+        d.n_layers = len(self.dims) - 1
+        for i, v in enumerate(self.dims):
+            d.dims[i] = v
+        d.params = _ptr(self.params)
+        return d
+
+    @property
+    def out_dim(self) -> int:
+        return int(self.dims[-1])
+
+
+@dataclass
+class DeviceQueries:
+    tex_id: torch.Tensor          # int32 view of uint32 [n]
+    uv: torch.Tensor              # float32 [n, 2]
+    mip: Optional[torch.Tensor]   # float32 [n] or None
+
+    @property
+    def n(self) -> int:
+        return int(self.tex_id.numel())
+
+    def struct(self) -> Queries:
+        q = Queries()
+        q.tex_id = _ptr(self.tex_id)
+        q.uv = _ptr(self.uv)
+        q.mip = _ptr(self.mip)
+        q.n = self.n
+        return q
+
+
+def _dev(a: np.ndarray, dtype, device) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a).view(dtype)).to(device)
+
+
+def upload(w, device="cuda"):
+    """Host workload (paper_2608_27888_amd.workloads.Workload) -> (DeviceModel, DeviceQueries)."""
+    model = DeviceModel(w.n_textures, list(w.res), list(w.channels),
+                        _dev(w.latents, np.int16, device), w.n_decoders, list(w.dims),
+                        _dev(w.params, np.int16, device), _dev(w.tex_to_dec, np.int32, device))
+    queries = DeviceQueries(_dev(w.tex_id, np.int32, device), _dev(w.uv, np.float32, device),
+                            None if w.mip is None else _dev(w.mip, np.float32, device))
+    return model, queries
+
+
+def decode(model: DeviceModel, queries: DeviceQueries, bins: Optional[Bins] = None,
+           out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Binned mode when `bins` is given, stream (divergent) mode otherwise."""
+    if out is None:
+        out = torch.empty((queries.n, model.out_dim), dtype=torch.float32,
+                          device=queries.tex_id.device)
+    g, d, q = model.grids(), model.decoders(), queries.struct()
+    if bins is not None:
+        st = lib().ntc_decode(ctypes.byref(g), ctypes.byref(d), _ptr(model.tex_to_dec),
+                              ctypes.byref(q), _ptr(bins.bin_offset), _ptr(bins.perm),
+                              bins.capacity, bins.align, _ptr(out), _stream(stream))
+    else:
+        st = lib().ntc_decode(ctypes.byref(g), ctypes.byref(d), _ptr(model.tex_to_dec),
+                              ctypes.byref(q), None, None, 0, 0, _ptr(out), _stream(stream))
+    _check("ntc_decode", st)
+    return out
+
+
+# ----------------------------------------------------------------------------- divergence
+
+
+def divergence_stats(tex_id: torch.Tensor, tex_to_dec: torch.Tensor, n_decoders: int,
+                     order: Optional[torch.Tensor] = None, wave: int = 64,
+                     n_textures: Optional[int] = None, stream=None):
+    """-> (per_wave_distinct int32 tensor, totals int64 tensor [4])."""
+    n = int(tex_id.numel())
+    T = int(tex_to_dec.numel()) if n_textures is None else int(n_textures)
+    ln = n if order is None else int(order.numel())
+    per = torch.empty(max(1, (ln + wave - 1) // wave), dtype=torch.int32, device=tex_id.device)
+    tot = torch.empty(4, dtype=torch.int64, device=tex_id.device)
+    _check("ntc_divergence_stats", lib().ntc_divergence_stats(
+        _ptr(tex_id), n, _ptr(tex_to_dec), T, n_decoders, _ptr(order), ln, wave, _ptr(per),
+        _ptr(tot), _stream(stream)))
+    return per[: (ln + wave - 1) // wave], tot

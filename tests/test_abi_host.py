@@ -1,0 +1,121 @@
+"""The C-ABI library loads, exports every entry point its header declares, and
+rejects malformed arguments on the host before any device work (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_27888_amd import ntc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ntc.h")
+
+FAKE = ctypes.c_void_p(0x100000)  # never dereferenced: validation fails first
+
+
+def declared_functions():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w \*]*?\b(ntc_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(ntc.LIB_PATH):
+        from paper_2608_27888_amd import build
+        build.build()
+    return ntc.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert {"ntc_build_bins", "ntc_decode", "ntc_divergence_stats"} <= set(names)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    assert ntc.status_string(0) == "ok"
+    for s in (-1, -2, -3, -4, -5):
+        assert ntc.status_string(s) not in ("ok", "unknown status")
+    assert ntc.status_string(7) == "unknown status"
+
+
+def test_sizes(L):
+    assert ntc.workspace_bytes(-1, 4) == 0
+    assert ntc.workspace_bytes(10, 0) == 0
+    assert ntc.workspace_bytes(10, 4097) == 0
+    assert ntc.workspace_bytes(1 << 23, 16) > 16 * 4
+    assert ntc.workspace_bytes(0, 1) > 0
+    assert ntc.perm_capacity(100, 16, 64) == 100 + 16 * 63
+    assert ntc.perm_capacity(100, 16, 1) == 100
+    assert ntc.perm_capacity(100, 16, 3) == -1
+    assert ntc.perm_capacity(100, 16, 8192) == -1
+
+
+def _bins(L, **kw):
+    a = dict(tex_id=FAKE, n=100, tex_to_dec=FAKE, T=4, D=2, align=64, cnt=FAKE, off=FAKE,
+             perm=FAKE, cap=100 + 2 * 63, ws=FAKE, wsb=1 << 20)
+    a.update(kw)
+    return L.ntc_build_bins(a["tex_id"], a["n"], a["tex_to_dec"], a["T"], a["D"], a["align"],
+                            a["cnt"], a["off"], a["perm"], a["cap"], a["ws"], a["wsb"], None)
+
+
+def test_build_bins_validation(L):
+    assert _bins(L, n=-1) == ntc.NTC_ERR_ARG
+    assert _bins(L, tex_id=None) == ntc.NTC_ERR_ARG
+    assert _bins(L, perm=None) == ntc.NTC_ERR_ARG
+    assert _bins(L, ws=None) == ntc.NTC_ERR_ARG
+    assert _bins(L, D=0) == ntc.NTC_ERR_ARG
+    assert _bins(L, D=4097) == ntc.NTC_ERR_ARG
+    assert _bins(L, T=0) == ntc.NTC_ERR_ARG
+    assert _bins(L, align=48) == ntc.NTC_ERR_ARG
+    assert _bins(L, cap=100 + 2 * 63 - 1) == ntc.NTC_ERR_CAPACITY
+    assert _bins(L, wsb=8) == ntc.NTC_ERR_CAPACITY
+    assert _bins(L, n=1 << 32) == ntc.NTC_ERR_ARG
+
+
+def _decode(L, res=(256, 128), ch=(16, 16), dims=(32, 64, 64, 8), n=100, D=4, binned=False,
+            align=64, cap=None, nulls=()):
+    g = ntc.Grids()
+    g.n_textures, g.n_levels = 4, len(res)
+    for i, (r, c) in enumerate(zip(res, ch)):
+        g.res[i], g.channels[i] = r, c
+    g.latents = None if "latents" in nulls else FAKE
+    d = ntc.Decoders()
+    d.n_decoders, d.n_layers = D, len(dims) - 1
+    for i, v in enumerate(dims):
+        d.dims[i] = v
+    d.params = None if "params" in nulls else FAKE
+    q = ntc.Queries()
+    q.tex_id, q.uv, q.mip, q.n = FAKE, FAKE, None, n
+    if cap is None:
+        cap = ntc.perm_capacity(max(n, 0), D, 64)
+    return L.ntc_decode(ctypes.byref(g), ctypes.byref(d), FAKE, ctypes.byref(q),
+                        FAKE if binned else None, FAKE if binned else None, cap, align,
+                        None if "out" in nulls else FAKE, None)
+
+
+def test_decode_validation(L):
+    assert _decode(L, n=-5) == ntc.NTC_ERR_ARG
+    assert _decode(L, nulls=("latents",)) == ntc.NTC_ERR_ARG
+    assert _decode(L, nulls=("out",)) == ntc.NTC_ERR_ARG
+    assert _decode(L, dims=(31, 64, 64, 8)) == ntc.NTC_ERR_ARG          # dims[0] != channels
+    assert _decode(L, dims=(32, 64, 48, 8)) == ntc.NTC_ERR_UNSUPPORTED  # unequal hidden widths
+    assert _decode(L, dims=(32, 96, 96, 8)) == ntc.NTC_ERR_UNSUPPORTED  # width not built
+    assert _decode(L, dims=(32, 64, 64, 20)) == ntc.NTC_ERR_UNSUPPORTED  # too many outputs
+    assert _decode(L, dims=(32, 8)) == ntc.NTC_ERR_UNSUPPORTED          # no hidden layer
+    assert _decode(L, res=(256, 128), ch=(16, 8), dims=(24, 64, 8)) == ntc.NTC_ERR_UNSUPPORTED
+    assert _decode(L, res=(0, 128)) == ntc.NTC_ERR_ARG
+    assert _decode(L, binned=True, align=32) == ntc.NTC_ERR_ARG
+    assert _decode(L, binned=True, cap=10) == ntc.NTC_ERR_CAPACITY
+    assert _decode(L, n=0) == ntc.NTC_OK  # nothing to do, nothing launched
+
+
+def test_divergence_validation(L):
+    f = L.ntc_divergence_stats
+    assert f(FAKE, 10, FAKE, 4, 2, None, 10, 0, FAKE, FAKE, None) == ntc.NTC_ERR_ARG
+    assert f(FAKE, 10, FAKE, 4, 2, None, 10, 65, FAKE, FAKE, None) == ntc.NTC_ERR_ARG
+    assert f(FAKE, 10, FAKE, 4, 2, None, 11, 64, FAKE, FAKE, None) == ntc.NTC_ERR_ARG
+    assert f(FAKE, 10, FAKE, 4, 2, None, 10, 64, FAKE, None, None) == ntc.NTC_ERR_ARG
+    assert f(FAKE, -1, FAKE, 4, 2, None, 0, 64, FAKE, FAKE, None) == ntc.NTC_ERR_ARG

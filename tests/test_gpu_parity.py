@@ -1,0 +1,183 @@
+"""GPU parity: the HIP library against the CPU oracle on the same seeded inputs.
+
+Binning (counts, offsets, permutation) and per-wave divergence counts must be
+bit-exact; decoded channels must lie within max-abs 2e-3 of the oracle's
+float64 values (the tolerance of the decode path: fp16 operands and fp16
+activations, fp32 accumulation).  Stream mode and binned mode must agree bit
+for bit, since a query's output depends on that query alone.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_27888_amd import ntc
+from paper_2608_27888_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+SMALL = ["tiny", "single", "divergent", "clustered4k", "clustered4k_d512", "wide_trilinear",
+         "wide_trilinear_d512"]
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    ntc.lib()
+    return torch.device("cuda:0")
+
+
+_cache = {}
+
+
+def small(name):
+    if name not in _cache:
+        _cache[name] = W.small(name)
+    return _cache[name]
+
+
+def u32(t):
+    return t.cpu().numpy().view(np.uint32)
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_bins_bit_exact(dev, oracle, name):
+    w = small(name)
+    say(f"[bins] {name} n={w.n} D={w.n_decoders}")
+    model, q = ntc.upload(w, dev)
+    bins = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders)
+    cnt, off, perm, bad = oracle.build_bins(w.tex_id, w.tex_to_dec, w.n_decoders, 64)
+    torch.cuda.synchronize()
+    assert np.array_equal(u32(bins.bin_count), cnt)
+    assert np.array_equal(u32(bins.bin_offset), off)
+    assert np.array_equal(u32(bins.perm)[: off[-1]], perm)
+    assert ntc.device_error(bins) == bad == 0
+
+
+@pytest.mark.parametrize("align", [1, 8, 64, 256])
+def test_bins_invalid_ids_and_alignments(dev, oracle, align):
+    rng = np.random.default_rng(align)
+    T, D, n = 37, 11, 70001
+    t2d = rng.integers(0, D + 1, T).astype(np.uint32)     # some textures map past D
+    tex = rng.integers(0, T + 3, n).astype(np.uint32)     # some ids past T
+    say(f"[bins-invalid] align={align} n={n}")
+    bins = ntc.build_bins(torch.from_numpy(tex.view(np.int32)).to(dev),
+                          torch.from_numpy(t2d.view(np.int32)).to(dev), D, align=align,
+                          n_textures=T)
+    cnt, off, perm, bad = oracle.build_bins(tex, t2d, D, align)
+    assert np.array_equal(u32(bins.bin_count), cnt)
+    assert np.array_equal(u32(bins.bin_offset), off)
+    assert np.array_equal(u32(bins.perm)[: off[-1]], perm)
+    assert bad > 0 and ntc.device_error(bins) == bad
+
+
+@pytest.mark.parametrize("n", [0, 1, 63, 64, 65, 8191, 8192, 8193])
+def test_bins_edge_sizes(dev, oracle, n):
+    rng = np.random.default_rng(n)
+    T, D = 9, 5
+    t2d = rng.integers(0, D, T).astype(np.uint32)
+    tex = rng.integers(0, T, n).astype(np.uint32)
+    say(f"[bins-edge] n={n}")
+    tex_d = torch.from_numpy(tex.view(np.int32)).to(dev) if n else torch.zeros(0, dtype=torch.int32, device=dev)
+    bins = ntc.build_bins(tex_d, torch.from_numpy(t2d.view(np.int32)).to(dev), D)
+    cnt, off, perm, _ = oracle.build_bins(tex, t2d, D, 64)
+    assert np.array_equal(u32(bins.bin_count), cnt)
+    assert np.array_equal(u32(bins.bin_offset), off)
+    assert np.array_equal(u32(bins.perm)[: off[-1]], perm)
+
+
+@pytest.mark.parametrize("name", SMALL)
+@pytest.mark.parametrize("wave", [64, 32])
+def test_divergence_bit_exact(dev, oracle, name, wave):
+    w = small(name)
+    say(f"[divergence] {name} wave={wave}")
+    model, q = ntc.upload(w, dev)
+    per, tot = ntc.divergence_stats(q.tex_id, model.tex_to_dec, w.n_decoders, wave=wave)
+    per_o, tot_o = oracle.divergence(w.tex_id, w.tex_to_dec, w.n_decoders, wave=wave)
+    assert np.array_equal(u32(per), per_o)
+    assert np.array_equal(tot.cpu().numpy().astype(np.uint64), tot_o)
+    bins = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders)
+    P = int(u32(bins.bin_offset)[-1])
+    perm_d = bins.perm[:P]
+    per_b, tot_b = ntc.divergence_stats(q.tex_id, model.tex_to_dec, w.n_decoders, order=perm_d,
+                                        wave=wave)
+    per_bo, tot_bo = oracle.divergence(w.tex_id, w.tex_to_dec, w.n_decoders,
+                                       order=u32(perm_d), wave=wave)
+    assert np.array_equal(u32(per_b), per_bo)
+    assert np.array_equal(tot_b.cpu().numpy().astype(np.uint64), tot_bo)
+    assert int(tot_b[3]) == 1  # binned order: one decoder per wave
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_decode_matches_oracle(dev, oracle, name):
+    w = small(name)
+    say(f"[decode] {name} n={w.n} dims={w.dims} levels={w.res}x{w.channels} mip={w.mip is not None}")
+    model, q = ntc.upload(w, dev)
+    bins = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders)
+    out_b = ntc.decode(model, q, bins)
+    out_s = ntc.decode(model, q)
+    ref = oracle.decode(w)
+    yb, ys = out_b.cpu().numpy(), out_s.cpu().numpy()
+    err = np.abs(yb.astype(np.float64) - ref).max()
+    say(f"    max abs err {err:.3e}")
+    assert err <= TOL
+    assert np.array_equal(yb.view(np.uint32), ys.view(np.uint32))  # modes agree bit for bit
+    assert np.all((yb >= 0) & (yb <= 1))
+
+
+def test_decode_is_deterministic(dev):
+    w = small("clustered4k")
+    say("[determinism] clustered4k")
+    model, q = ntc.upload(w, dev)
+    b1 = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders)
+    o1 = ntc.decode(model, q, b1).clone()
+    b2 = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders)
+    o2 = ntc.decode(model, q, b2)
+    P = int(u32(b1.bin_offset)[-1])
+    assert torch.equal(b1.bin_offset, b2.bin_offset)
+    assert torch.equal(b1.perm[:P], b2.perm[:P])  # slots past P are never written
+    assert torch.equal(o1.view(torch.int32), o2.view(torch.int32))
+
+
+def test_decode_invalid_queries_untouched(dev, oracle):
+    w = W.small("tiny")
+    w.tex_id = w.tex_id.copy()
+    w.tex_id[::13] = 7                         # past the last texture
+    w.tex_to_dec = np.array([0, 1, 0, 9], np.uint32)  # texture 3 maps past the last decoder
+    say("[invalid] tiny with bad ids")
+    model, q = ntc.upload(w, dev)
+    sentinel = -12345.0
+    out_s = torch.full((w.n, w.out_dim), sentinel, device=dev)
+    ntc.decode(model, q, out=out_s)
+    bins = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders)
+    out_b = torch.full((w.n, w.out_dim), sentinel, device=dev)
+    ntc.decode(model, q, bins, out=out_b)
+    ref = oracle.decode(w)
+    bad = np.isnan(ref[:, 0])
+    assert bad.sum() > 0 and ntc.device_error(bins) == int(bad.sum())
+    for o in (out_s.cpu().numpy(), out_b.cpu().numpy()):
+        assert np.all(o[bad] == sentinel)
+        assert np.abs(o[~bad] - ref[~bad]).max() <= TOL
+
+
+def test_decode_texel_centres_and_far_uv(dev, oracle):
+    """Queries exactly at texel centres, on edges and far outside [0, 1)."""
+    w = W.small("single")
+    rng = np.random.default_rng(1)
+    n = 5000
+    r = w.res[0]
+    ix, iy = rng.integers(0, r, n), rng.integers(0, r, n)
+    uv = np.stack([(ix + 0.5) / r, (iy + 0.5) / r], 1).astype(np.float32)
+    uv[:500] = rng.uniform(-50, 50, (500, 2)).astype(np.float32)
+    uv[500:600] = np.array([0.0, 1.0], np.float32)[rng.integers(0, 2, (100, 2))]
+    w.uv, w.tex_id = np.ascontiguousarray(uv), np.zeros(n, np.uint32)
+    say("[texel-centres]")
+    model, q = ntc.upload(w, dev)
+    out = ntc.decode(model, q).cpu().numpy()
+    assert np.abs(out - oracle.decode(w)).max() <= TOL
