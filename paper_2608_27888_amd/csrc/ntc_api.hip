@@ -86,8 +86,9 @@ int ntc_decode(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex_to
   for (int l = 0; l < L; ++l) {
     const int r = g->res[l];
     if (r < 1 || r > 16384 || g->channels[l] < 1) return NTC_ERR_ARG;
+    if (r < 2) return NTC_ERR_UNSUPPORTED;  // the gather addresses a 2x2 quad
     if (g->channels[l] != ch) return NTC_ERR_UNSUPPORTED;
-    a.level_off[l] = (int32_t)tex_stride;
+    a.level_off[l] = (uint32_t)tex_stride;
     a.res[l] = r;
     a.resf[l] = (float)r;
     tex_stride += (int64_t)r * r * ch;
@@ -104,7 +105,9 @@ int ntc_decode(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex_to
   for (int i = 1; i < nl; ++i)
     if (m->dims[i] != hid) return NTC_ERR_UNSUPPORTED;
   const int out_dim = m->dims[nl];
-  if (out_dim > 16) return NTC_ERR_UNSUPPORTED;
+  if (out_dim > 16 || out_dim % 4 != 0) return NTC_ERR_UNSUPPORTED;
+  // one buffer resource with 32-bit byte offsets covers the output
+  if (q->n * (int64_t)out_dim * 4 > 0x7FFFFFF0LL) return NTC_ERR_UNSUPPORTED;
   int64_t dec_stride = 0;
   for (int i = 0; i < nl; ++i) dec_stride += (int64_t)m->dims[i + 1] * (m->dims[i] + 1);
 

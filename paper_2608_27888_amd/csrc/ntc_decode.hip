@@ -39,14 +39,16 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float float2v __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short short2v __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kMaxHidden = 3;  // hidden -> hidden layers
 
+// Two floats -> packed fp16 pair, round to nearest even (one v_cvt_pk_f16_f32).
 __device__ __forceinline__ uint32_t pack_half2(float a, float b) {
-  half2v h = {(_Float16)a, (_Float16)b};  // round to nearest even
-  return __builtin_bit_cast(uint32_t, h);
+  const float2v f = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, half2v));
 }
 
 __device__ __forceinline__ half8 as_half8(u32x4 v) { return __builtin_bit_cast(half8, v); }
@@ -194,41 +196,51 @@ struct Query {
 };
 
 // Bilinear sample of one level: CH fp32 values, weights in fp32, latents fed
-// to mixed-precision FMAs as fp16.
+// to mixed-precision FMAs as fp16.  The lower tap is clamped to [0, res - 2]
+// and the weight to [0, 1]; for res >= 2 this is exactly bilinear filtering
+// with both taps clamped to the edge, and it puts the right-hand tap 2*CH bytes
+// after the left one (an immediate offset) and the lower row res*CH values
+// further on.  Any finite or NaN coordinate keeps every tap inside the level.
+// The 2x2 texels of one level around a query and its position between them.
 template <int CH>
-__device__ __forceinline__ void sample_level(const uint16_t *level, int res, float resf, float u,
-                                             float v, float *f) {
+struct LevelTaps {
+  static constexpr int NV = CH / 8;  // 16-byte vectors per texel
+  u32x4 t00[NV], t10[NV], t01[NV], t11[NV];
+  float fx, fy;
+};
+
+template <int CH>
+__device__ __forceinline__ void fetch_level(const uint16_t *tex, uint32_t level_off, int res,
+                                            float resf, float u, float v, LevelTaps<CH> &L) {
   const float x = __builtin_fmaf(u, resf, -0.5f), y = __builtin_fmaf(v, resf, -0.5f);
-  const float x0f = __builtin_floorf(x), y0f = __builtin_floorf(y);
-  const float fx = x - x0f, fy = y - y0f;
-  // bound before converting so that any finite (or NaN) coordinate stays in range
-  const int xi = (int)__builtin_fminf(__builtin_fmaxf(x0f, -1.f), resf);
-  const int yi = (int)__builtin_fminf(__builtin_fmaxf(y0f, -1.f), resf);
-  // xi, yi in [-1, res]: both taps clamp into [0, res - 1] (clamp-to-edge)
-  const int x0 = min(max(xi, 0), res - 1), x1 = min(max(xi + 1, 0), res - 1);
-  const int y0 = min(max(yi, 0), res - 1), y1 = min(max(yi + 1, 0), res - 1);
-  const float w00 = (1.f - fx) * (1.f - fy), w10 = fx * (1.f - fy);
-  const float w01 = (1.f - fx) * fy, w11 = fx * fy;
-  const u32x4 *t00 = (const u32x4 *)(level + ((size_t)(y0 * res + x0)) * CH);
-  const u32x4 *t10 = (const u32x4 *)(level + ((size_t)(y0 * res + x1)) * CH);
-  const u32x4 *t01 = (const u32x4 *)(level + ((size_t)(y1 * res + x0)) * CH);
-  const u32x4 *t11 = (const u32x4 *)(level + ((size_t)(y1 * res + x1)) * CH);
-  constexpr int NV = CH / 8;  // 16-byte vectors per texel
-  u32x4 l00[NV], l10[NV], l01[NV], l11[NV];
+  const float hi = resf - 2.f;
+  const float x0 = __builtin_fminf(__builtin_fmaxf(__builtin_floorf(x), 0.f), hi);
+  const float y0 = __builtin_fminf(__builtin_fmaxf(__builtin_floorf(y), 0.f), hi);
+  L.fx = __builtin_fminf(__builtin_fmaxf(x - x0, 0.f), 1.f);
+  L.fy = __builtin_fminf(__builtin_fmaxf(y - y0, 0.f), 1.f);
+  const uint32_t idx = level_off + ((uint32_t)y0 * (uint32_t)res + (uint32_t)x0) * CH;
+  const u32x4 *r0 = (const u32x4 *)(tex + idx);
+  const u32x4 *r1 = (const u32x4 *)(tex + idx + (uint32_t)res * CH);
 #pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    l00[i] = t00[i];
-    l10[i] = t10[i];
-    l01[i] = t01[i];
-    l11[i] = t11[i];
+  for (int i = 0; i < LevelTaps<CH>::NV; ++i) {
+    L.t00[i] = r0[i];
+    L.t10[i] = r0[LevelTaps<CH>::NV + i];
+    L.t01[i] = r1[i];
+    L.t11[i] = r1[LevelTaps<CH>::NV + i];
   }
+}
+
+template <int CH>
+__device__ __forceinline__ void interp_level(const LevelTaps<CH> &L, float *f) {
+  const float gx = 1.f - L.fx, gy = 1.f - L.fy;
+  const float w00 = gx * gy, w10 = L.fx * gy, w01 = gx * L.fy, w11 = L.fx * L.fy;
 #pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const half8 a = as_half8(l00[i]), b = as_half8(l10[i]);
-    const half8 c = as_half8(l01[i]), d = as_half8(l11[i]);
+  for (int i = 0; i < LevelTaps<CH>::NV; ++i) {
+    const half8 a = as_half8(L.t00[i]), b = as_half8(L.t10[i]);
+    const half8 c = as_half8(L.t01[i]), d = as_half8(L.t11[i]);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      float s = w00 * (float)a[e];
+      float s = __builtin_fmaf(w00, (float)a[e], 0.f);
       s = __builtin_fmaf(w10, (float)b[e], s);
       s = __builtin_fmaf(w01, (float)c[e], s);
       s = __builtin_fmaf(w11, (float)d[e], s);
@@ -237,17 +249,24 @@ __device__ __forceinline__ void sample_level(const uint16_t *level, int res, flo
   }
 }
 
-template <int NL>
-__device__ __forceinline__ int pick(const int32_t (&v)[NTC_MAX_LEVELS], int k) {
-  int r = v[0];
-#pragma unroll
-  for (int i = 1; i < NL; ++i) r = k == i ? v[i] : r;
-  return r;
+// Bilinear sample of one level: CH fp32 values, weights in fp32, latents fed
+// to mixed-precision FMAs as fp16.  The lower tap is clamped to [0, res - 2]
+// and the weight to [0, 1]; for res >= 2 this is exactly bilinear filtering
+// with both taps clamped to the edge, and it puts the right-hand tap 2*CH bytes
+// after the left one (an immediate offset) and the lower row res*CH values
+// further on.  Any finite or NaN coordinate keeps every tap inside the level.
+template <int CH>
+__device__ __forceinline__ void sample_level(const uint16_t *tex, uint32_t level_off, int res,
+                                             float resf, float u, float v, float *f) {
+  LevelTaps<CH> L;
+  fetch_level<CH>(tex, level_off, res, resf, u, v, L);
+  interp_level<CH>(L, f);
 }
 
-template <int NL>
-__device__ __forceinline__ float pickf(const float (&v)[NTC_MAX_LEVELS], int k) {
-  float r = v[0];
+// v[k] for a per-lane level index k < NL, as a chain of selects (no scratch).
+template <int NL, typename T>
+__device__ __forceinline__ T pick(const T (&v)[NTC_MAX_LEVELS], int k) {
+  T r = v[0];
 #pragma unroll
   for (int i = 1; i < NL; ++i) r = k == i ? v[i] : r;
   return r;
@@ -263,23 +282,50 @@ __device__ __forceinline__ void gather(const DecodeArgs &a, const Query &qq,
   for (int l = 0; l < NL; ++l) {
     float f[CH];
     if (!MIP) {
-      sample_level<CH>(tex + a.level_off[l], a.res[l], a.resf[l], qq.u, qq.v, f);
+      sample_level<CH>(tex, a.level_off[l], a.res[l], a.resf[l], qq.u, qq.v, f);
     } else {
       float m = __builtin_fminf(__builtin_fmaxf(qq.mip, 0.f), (float)(NL - 1));
       const float lod = __builtin_fmaxf((float)l, m);
       const int k0 = (int)__builtin_floorf(lod);
       const int k1 = min(k0 + 1, NL - 1);
       const float t = lod - (float)k0;
-      sample_level<CH>(tex + pick<NL>(a.level_off, k0), pick<NL>(a.res, k0),
-                       pickf<NL>(a.resf, k0), qq.u, qq.v, f);
+      sample_level<CH>(tex, pick<NL>(a.level_off, k0), pick<NL>(a.res, k0),
+                       pick<NL>(a.resf, k0), qq.u, qq.v, f);
       if (__builtin_amdgcn_ballot_w64(t != 0.f)) {
         float g[CH];
-        sample_level<CH>(tex + pick<NL>(a.level_off, k1), pick<NL>(a.res, k1),
-                         pickf<NL>(a.resf, k1), qq.u, qq.v, g);
+        sample_level<CH>(tex, pick<NL>(a.level_off, k1), pick<NL>(a.res, k1),
+                         pick<NL>(a.resf, k1), qq.u, qq.v, g);
 #pragma unroll
         for (int c = 0; c < CH; ++c) f[c] = __builtin_fmaf(t, g[c] - f[c], f[c]);
       }
     }
+#pragma unroll
+    for (int c = 0; c < CH; c += 2) x[(l * CH + c) / 2] = pack_half2(f[c], f[c + 1]);
+  }
+}
+
+// Taps of all levels of one query, for the pipelined path without mip.
+template <int NL, int CH>
+struct TileTaps {
+  LevelTaps<CH> lv[NL];
+};
+
+template <int NL, int CH>
+__device__ __forceinline__ void fetch_taps(const DecodeArgs &a, const Query &qq,
+                                           TileTaps<NL, CH> &T) {
+  const uint16_t *tex = a.latents + (size_t)qq.tex * (size_t)a.tex_stride;
+#pragma unroll
+  for (int l = 0; l < NL; ++l)
+    fetch_level<CH>(tex, a.level_off[l], a.res[l], a.resf[l], qq.u, qq.v, T.lv[l]);
+}
+
+template <int NL, int CH>
+__device__ __forceinline__ void interp_taps(const TileTaps<NL, CH> &T,
+                                            uint32_t (&x)[NL * CH / 2]) {
+#pragma unroll
+  for (int l = 0; l < NL; ++l) {
+    float f[CH];
+    interp_level<CH>(T.lv[l], f);
 #pragma unroll
     for (int c = 0; c < CH; c += 2) x[(l * CH + c) / 2] = pack_half2(f[c], f[c + 1]);
   }
@@ -309,14 +355,21 @@ __device__ __forceinline__ void to_b_operands(const uint32_t (&x)[KS * 8], half8
   }
 }
 
+// fp16 pair (round to nearest even) with ReLU applied on the packed halves: a
+// negative half has its sign bit set, so a signed 16-bit max with 0 zeroes it.
+// Rounding commutes with ReLU, so this equals rounding ReLU(x).
+__device__ __forceinline__ uint32_t relu_pack2(float a, float b) {
+  const short2v h = __builtin_bit_cast(short2v, pack_half2(a, b));
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(h, short2v{0, 0}));
+}
+
 // ReLU + fp16 of one 32-row output block -> two K-slices of the next layer.
 __device__ __forceinline__ void relu_pack(const floatx16 &acc, half8 &s0, half8 &s1) {
   u32x4 a, b;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    a[i] = pack_half2(__builtin_fmaxf(acc[2 * i], 0.f), __builtin_fmaxf(acc[2 * i + 1], 0.f));
-    b[i] = pack_half2(__builtin_fmaxf(acc[8 + 2 * i], 0.f),
-                      __builtin_fmaxf(acc[8 + 2 * i + 1], 0.f));
+    a[i] = relu_pack2(acc[2 * i], acc[2 * i + 1]);
+    b[i] = relu_pack2(acc[8 + 2 * i], acc[8 + 2 * i + 1]);
   }
   s0 = as_half8(a);
   s1 = as_half8(b);
@@ -328,13 +381,13 @@ __device__ __forceinline__ float sigmoid(float z) {
 
 // Runs the staged decoder on the tile's features; returns the output layer's
 // accumulators (sigmoid applied) for the two column blocks.
-template <int NL, int CH, int HID>
-__device__ __forceinline__ void run_mlp(const uint32_t *lds, int n_hidden,
+template <int NL, int CH, int HID, int NH>
+__device__ __forceinline__ void run_mlp(const uint32_t *lds,
                                         const half8 (&xb0)[NL * CH / 16],
                                         const half8 (&xb1)[NL * CH / 16], floatx16 &y0,
                                         floatx16 &y1) {
   using S = Shape<NL, CH, HID>;
-  const float *bias = (const float *)(lds) + image_of<NL, CH, HID>(n_hidden).bias_off;
+  const float *bias = (const float *)(lds) + image_of<NL, CH, HID>(NH).bias_off;
   half8 h0[S::KSH], h1[S::KSH];
   // layer 0: F -> HID
 #pragma unroll
@@ -352,7 +405,8 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds, int n_hidden,
   int frag = S::MB * S::KS0;
   const float *bl = bias + HID;
   // hidden -> hidden
-  for (int layer = 0; layer < n_hidden; ++layer) {
+#pragma unroll
+  for (int layer = 0; layer < NH; ++layer) {
     half8 n0[S::KSH], n1[S::KSH];
 #pragma unroll
     for (int mb = 0; mb < S::MB; ++mb) {
@@ -374,8 +428,9 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds, int n_hidden,
     frag += S::MB * S::KSH;
     bl += HID;
   }
-  // output layer: HID -> out (rows padded to 32)
-  floatx16 c0 = bias_frag(bl, 0), c1 = c0;
+  // output layer: HID -> out (rows padded to 32); the accumulator starts at
+  // zero and the bias of the rows this lane keeps is added by the epilogue
+  floatx16 c0 = {}, c1 = {};
 #pragma unroll
   for (int s = 0; s < S::KSH; ++s) {
     const half8 w = a_frag(lds, frag + s);
@@ -386,58 +441,123 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds, int n_hidden,
   y1 = c1;
 }
 
-// Sigmoid and store of the output rows held by this lane for column block nb.
-__device__ __forceinline__ void store_out(float *out, int out_dim, uint32_t q, bool ok,
-                                          const floatx16 &z) {
-  if (!ok) return;
+// Bias of the output rows 8g + 4h + r this lane holds, for the groups g the
+// output width reaches.
+__device__ __forceinline__ floatx16 out_bias(const uint32_t *lds, const Image &im, int hid,
+                                             int n_hidden, int out_dim) {
+  const float *bl = (const float *)lds + im.bias_off + hid * (1 + n_hidden);
   const int h = lane_id() >> 5;
-  float *row = out + (size_t)q * out_dim;
+  floatx16 b = {};
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    const int r0 = 8 * g + 4 * h;
-    if (r0 >= out_dim) continue;
-    float y[4];
+    if (8 * g >= out_dim) break;
+    const floatx4 v = *(const floatx4 *)(bl + 8 * g + 4 * h);
+    b[4 * g + 0] = v[0];
+    b[4 * g + 1] = v[1];
+    b[4 * g + 2] = v[2];
+    b[4 * g + 3] = v[3];
+  }
+  return b;
+}
+
+// Raw buffer resource over the output rows: a store whose byte offset lies past
+// the range is dropped by the hardware, so masked lanes need no branch and
+// every path issues the same number of stores.
+constexpr uint32_t kDropOffset = 0x80000000u;  // past any output range (< 2 GiB)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t out_resource(const DecodeArgs &a) {
+  return __builtin_amdgcn_make_buffer_rsrc(a.out, 0, (int)(a.n * (uint32_t)a.out_dim * 4u),
+                                           0x00020000);
+}
+
+// Bias, sigmoid and store of the output rows held by this lane (rows 8g + 4h + r
+// of the query in its column), as 16-byte stores; the output width is a
+// multiple of 4.  The loop bound depends on the output width only, so no lane
+// computes rows past it.
+__device__ __forceinline__ void store_out(__amdgpu_buffer_rsrc_t out, int out_dim, uint32_t q,
+                                          bool ok, const floatx16 &z, const floatx16 &bias) {
+  const int h = lane_id() >> 5;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) y[r] = sigmoid(z[4 * g + r]);
-    if (r0 + 4 <= out_dim && (out_dim & 3) == 0) {
-      *(floatx4 *)(row + r0) = floatx4{y[0], y[1], y[2], y[3]};
-    } else {
-      for (int r = 0; r < 4 && r0 + r < out_dim; ++r) row[r0 + r] = y[r];
-    }
+  for (int g = 0; g < 4; ++g) {
+    if (8 * g >= out_dim) break;
+    u32x4 y;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      y[r] = __builtin_bit_cast(uint32_t, sigmoid(z[4 * g + r] + bias[4 * g + r]));
+    const int r0 = 8 * g + 4 * h;
+    const uint32_t off =
+        ok && r0 < out_dim ? (q * (uint32_t)out_dim + (uint32_t)r0) * 4u : kDropOffset;
+    __builtin_amdgcn_raw_buffer_store_b128(y, out, off, 0, 0);
   }
 }
 
+// Query data of a slot.  The loads are unconditional (a slot without a valid
+// query reads query 0 and is marked invalid), so every wave issues the same
+// number of loads on every path and waits stay exact; the texture id is
+// checked once it has arrived.
 template <int NL, bool MIP>
 __device__ __forceinline__ Query load_query(const DecodeArgs &a, uint32_t q, bool in_range) {
   Query r;
   r.q = q;
-  r.valid = in_range && q < a.n;
-  r.tex = r.valid ? a.tex_id[q] : 0u;
-  r.valid = r.valid && r.tex < (uint32_t)a.n_textures;
+  const bool ok = in_range && q < a.n;
+  const uint32_t qs = ok ? q : 0u;
+  r.tex = a.tex_id[qs];
+  const float2 uv = ((const float2 *)a.uv)[qs];
+  r.u = uv.x;
+  r.v = uv.y;
+  r.mip = MIP ? a.mip[qs] : 0.f;
+  r.valid = ok && r.tex < (uint32_t)a.n_textures;
   if (!r.valid) r.tex = 0;
-  r.u = 0.f;
-  r.v = 0.f;
-  r.mip = 0.f;
-  if (r.valid) {
-    const float2 uv = ((const float2 *)a.uv)[q];
-    r.u = uv.x;
-    r.v = uv.y;
-    if (MIP) r.mip = a.mip[q];
-  }
   return r;
 }
 
 // ------------------------------------------------------------------- kernels
 
-template <int NL, int CH, int HID, bool MIP>
-__global__ void __launch_bounds__(kBlock)
+typedef const __attribute__((address_space(4))) uint32_t *const_u32p;
+
+// Wave-uniform read of the bin offsets through the constant address space, so
+// it becomes a scalar load that does not enter the vector-memory counter.
+__device__ __forceinline__ uint32_t bin_off(const DecodeArgs &a, uint32_t i) {
+  return ((const_u32p)a.bin_offset)[i];
+}
+
+// A group of up to four consecutive tiles of one bin: tiles [t, t + n) of bin d,
+// whose tiles end at be.  n == 0 marks the end of a workgroup's range.
+struct Group {
+  uint32_t t, n, d, be;
+};
+
+__device__ __forceinline__ Group group_at(const DecodeArgs &a, uint32_t t, uint32_t d,
+                                          uint32_t be, uint32_t D, uint32_t t_end) {
+  while (t >= be && d + 1 < D) {  // next non-empty bin
+    ++d;
+    be = bin_off(a, d + 1) / kWave;
+  }
+  const uint32_t n =
+      (t >= be || t >= t_end) ? 0u : min(min((uint32_t)kWavesPerBlock, be - t), t_end - t);
+  return Group{t, n, d, be};
+}
+
+__device__ __forceinline__ Group next_group(const DecodeArgs &a, const Group &g, uint32_t D,
+                                            uint32_t t_end) {
+  return g.n ? group_at(a, g.t + g.n, g.d, g.be, D, t_end) : g;
+}
+
+// Workgroups per CU the register allocation must allow: 4 (4 waves per SIMD,
+// <= 128 VGPRs) for 64-wide decoders, 2 for 128-wide ones.
+template <int HID>
+constexpr int kMinBlocks = HID <= 64 ? 4 : 2;
+
+template <int NL, int CH, int HID, int NH, bool MIP>
+__global__ void __launch_bounds__(kBlock, kMinBlocks<HID>)
 decode_binned(const DecodeArgs a) {
   using S = Shape<NL, CH, HID>;
   extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
   const uint32_t w = threadIdx.x / kWave, lane = lane_id();
   const uint32_t D = (uint32_t)a.n_decoders;
+  const __amdgpu_buffer_rsrc_t out_rsrc = out_resource(a);
   // tiles of the permutation; never more than the buffer holds
-  const uint64_t slots = min((uint64_t)a.bin_offset[D], a.perm_capacity);
+  const uint64_t slots = min((uint64_t)bin_off(a, D), a.perm_capacity);
   const uint32_t total_tiles = (uint32_t)(slots / kWave);
   const uint32_t per = (total_tiles + gridDim.x - 1) / gridDim.x;
   const uint32_t blk = xcd_local_block(blockIdx.x, gridDim.x);
@@ -448,49 +568,77 @@ decode_binned(const DecodeArgs a) {
   uint32_t lo = 0, hi = D;  // invariant: bin_offset[lo] <= 64 t < bin_offset[hi]
   while (hi - lo > 1) {
     const uint32_t mid = (lo + hi) / 2;
-    if (a.bin_offset[mid] <= t * kWave) lo = mid; else hi = mid;
+    if (bin_off(a, mid) <= t * kWave) lo = mid; else hi = mid;
   }
-  uint32_t d = lo, bin_end = a.bin_offset[d + 1] / kWave;
+  // Tiles go in groups of up to four consecutive tiles of one bin, tile t + w to
+  // wave w; every wave walks the same (uniform) sequence of groups.
+  Group g0 = group_at(a, t, lo, bin_off(a, lo + 1) / kWave, D, t_end);
+  Group g1 = next_group(a, g0, D, t_end);
+  Group g2 = next_group(a, g1, D, t_end);
+  // perm entry of this wave's tile in group g (NTC_PAD when the wave has none);
+  // the load itself is unconditional (slot 0 exists whenever there is a tile)
+  auto slot_query = [&](const Group &g) -> uint32_t {
+    const bool has = w < g.n;
+    const uint32_t v = a.perm[has ? (g.t + w) * kWave + lane : 0u];
+    return has ? v : NTC_PAD;
+  };
   uint32_t staged = 0xFFFFFFFFu;
-  while (t < t_end) {
-    while (t >= bin_end && d + 1 < D) {  // next non-empty bin
-      ++d;
-      bin_end = a.bin_offset[d + 1] / kWave;
-    }
-    if (t >= bin_end) break;  // offsets not ascending: nothing sensible left to do
-    const uint32_t group = min(min((uint32_t)kWavesPerBlock, bin_end - t), t_end - t);
-    if (d != staged) {
+  // Software pipeline, uniform across waves (a wave without a tile in a group
+  // runs it with every lane masked): while tile k is gathered and decoded, the
+  // query data of tile k+1 and the permutation entry of tile k+2 are in
+  // flight.  Loads are issued in the order they are consumed, so each wait only
+  // drains the oldest loads.
+  Query q0 = load_query<NL, MIP>(a, slot_query(g0), true);
+  uint32_t p1 = slot_query(g1);
+  while (g0.n) {
+    if (g0.d != staged) {
       __syncthreads();
-      stage_decoder<NL, CH, HID>(a, d, lds);
+      stage_decoder<NL, CH, HID>(a, g0.d, lds);
       __syncthreads();
-      staged = d;
+      staged = g0.d;
     }
-    if (w < group) {
-      const uint32_t slot = (t + w) * kWave + lane;
-      const Query qq = load_query<NL, MIP>(a, a.perm[slot], true);
-      uint32_t x[S::F / 2];
-      gather<NL, CH, MIP>(a, qq, x);
-      half8 xb0[S::KS0], xb1[S::KS0];
-      to_b_operands<S::KS0>(x, xb0, xb1);
-      floatx16 y0, y1;
-      run_mlp<NL, CH, HID>(lds, a.n_hidden, xb0, xb1, y0, y1);
-      const uint32_t q_other = (uint32_t)__shfl_xor((int)qq.q, 32, kWave);
-      const bool ok_other = __shfl_xor((int)qq.valid, 32, kWave) != 0;
-      const bool h = lane >= 32;
-      store_out(a.out, a.out_dim, h ? q_other : qq.q, h ? ok_other : qq.valid, y0);
-      store_out(a.out, a.out_dim, h ? qq.q : q_other, h ? qq.valid : ok_other, y1);
+    uint32_t x[S::F / 2];
+    Query q1;
+    uint32_t p2;
+    if constexpr (MIP) {
+      q1 = load_query<NL, MIP>(a, p1, true);
+      p2 = slot_query(g2);
+      gather<NL, CH, MIP>(a, q0, x);
+    } else {
+      TileTaps<NL, CH> taps;
+      fetch_taps<NL, CH>(a, q0, taps);
+      q1 = load_query<NL, MIP>(a, p1, true);
+      p2 = slot_query(g2);
+      // all loads above are issued before any of them is waited on
+      __builtin_amdgcn_sched_barrier(0);
+      interp_taps<NL, CH>(taps, x);
     }
-    t += group;
+    half8 xb0[S::KS0], xb1[S::KS0];
+    to_b_operands<S::KS0>(x, xb0, xb1);
+    floatx16 y0, y1;
+    run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, y0, y1);
+    const uint32_t q_other = (uint32_t)__shfl_xor((int)q0.q, 32, kWave);
+    const bool ok_other = __shfl_xor((int)q0.valid, 32, kWave) != 0;
+    const bool h = lane >= 32;
+    const floatx16 ob = out_bias(lds, image_of<NL, CH, HID>(NH), HID, NH, a.out_dim);
+    store_out(out_rsrc, a.out_dim, h ? q_other : q0.q, h ? ok_other : q0.valid, y0, ob);
+    store_out(out_rsrc, a.out_dim, h ? q0.q : q_other, h ? q0.valid : ok_other, y1, ob);
+    q0 = q1;
+    p1 = p2;
+    g0 = g1;
+    g1 = g2;
+    g2 = next_group(a, g2, D, t_end);
   }
 }
 
-template <int NL, int CH, int HID, bool MIP>
-__global__ void __launch_bounds__(kBlock)
+template <int NL, int CH, int HID, int NH, bool MIP>
+__global__ void __launch_bounds__(kBlock, kMinBlocks<HID>)
 decode_stream(const DecodeArgs a) {
   using S = Shape<NL, CH, HID>;
   extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
   __shared__ uint32_t next_dec[2][kWavesPerBlock];
   const uint32_t w = threadIdx.x / kWave, lane = lane_id();
+  const __amdgpu_buffer_rsrc_t out_rsrc = out_resource(a);
   const uint32_t n_tiles = (a.n + kWave - 1) / kWave;
   const uint32_t n_groups = (n_tiles + kWavesPerBlock - 1) / kWavesPerBlock;
   const uint32_t per = (n_groups + gridDim.x - 1) / gridDim.x;
@@ -534,10 +682,12 @@ decode_stream(const DecodeArgs a) {
       const uint64_t sel = ballot(mine_now);
       if (sel) {
         floatx16 y0, y1;
-        run_mlp<NL, CH, HID>(lds, a.n_hidden, xb0, xb1, y0, y1);
+        run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, y0, y1);
         const bool sel_other = __shfl_xor((int)mine_now, 32, kWave) != 0;
-        store_out(a.out, a.out_dim, h ? q_other : q, h ? sel_other : mine_now, y0);
-        store_out(a.out, a.out_dim, h ? q : q_other, h ? mine_now : sel_other, y1);
+        const floatx16 ob = out_bias(lds, image_of<NL, CH, HID>(NH), HID, NH,
+                                     a.out_dim);
+        store_out(out_rsrc, a.out_dim, h ? q_other : q, h ? sel_other : mine_now, y0, ob);
+        store_out(out_rsrc, a.out_dim, h ? q : q_other, h ? mine_now : sel_other, y1, ob);
         todo &= ~sel;
         live = live && !mine_now;
       }
@@ -545,43 +695,52 @@ decode_stream(const DecodeArgs a) {
   }
 }
 
-template <int NL, int CH, int HID, bool MIP>
+template <int NL, int CH, int HID, int NH, bool MIP>
 int launch_shape(const DecodeArgs &a, hipStream_t stream) {
-  const Image im = image_of<NL, CH, HID>(a.n_hidden);
+  const Image im = image_of<NL, CH, HID>(NH);
   const size_t lds = (size_t)im.bytes;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess)
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  const void *fn = a.bin_offset ? (const void *)decode_binned<NL, CH, HID, MIP>
-                                : (const void *)decode_stream<NL, CH, HID, MIP>;
+  const void *fn = a.bin_offset ? (const void *)decode_binned<NL, CH, HID, NH, MIP>
+                                : (const void *)decode_stream<NL, CH, HID, NH, MIP>;
   if (lds > 64 * 1024) {
     if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
         hipSuccess)
       return NTC_ERR_HIP;
   }
-  if (a.bin_offset) {
-    uint64_t blocks = ((uint64_t)a.max_tiles + kWavesPerBlock - 1) / kWavesPerBlock;
-    const uint64_t cap = (uint64_t)cus * 4;
-    if (blocks > cap) blocks = cap;
-    if (blocks == 0) return NTC_OK;
-    hipLaunchKernelGGL((decode_binned<NL, CH, HID, MIP>), dim3((unsigned)blocks), dim3(kBlock),
-                       lds, stream, a);
-  } else {
-    const uint64_t tiles = ((uint64_t)a.n + kWave - 1) / kWave;
-    uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
-    const uint64_t cap = (uint64_t)cus * 4;
-    if (blocks > cap) blocks = cap;
-    if (blocks == 0) return NTC_OK;
-    hipLaunchKernelGGL((decode_stream<NL, CH, HID, MIP>), dim3((unsigned)blocks), dim3(kBlock),
-                       lds, stream, a);
-  }
+  // every workgroup resident at once: one round, no tail of late workgroups
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, lds) != hipSuccess ||
+      per_cu < 1)
+    per_cu = 1;
+  const uint64_t cap = (uint64_t)cus * (uint64_t)per_cu;
+  const uint64_t tiles = a.bin_offset ? (uint64_t)a.max_tiles : ((uint64_t)a.n + kWave - 1) / kWave;
+  uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+  if (blocks > cap) blocks = cap;
+  if (blocks == 0) return NTC_OK;
+  if (a.bin_offset)
+    hipLaunchKernelGGL((decode_binned<NL, CH, HID, NH, MIP>), dim3((unsigned)blocks),
+                       dim3(kBlock), lds, stream, a);
+  else
+    hipLaunchKernelGGL((decode_stream<NL, CH, HID, NH, MIP>), dim3((unsigned)blocks),
+                       dim3(kBlock), lds, stream, a);
   return hip_status(hipGetLastError());
 }
 
-template <int NL, int CH, int HID>
+template <int NL, int CH, int HID, int NH>
 int launch_mip(const DecodeArgs &a, hipStream_t stream) {
-  return a.mip ? launch_shape<NL, CH, HID, true>(a, stream)
-               : launch_shape<NL, CH, HID, false>(a, stream);
+  return a.mip ? launch_shape<NL, CH, HID, NH, true>(a, stream)
+               : launch_shape<NL, CH, HID, NH, false>(a, stream);
+}
+
+template <int NL, int CH, int HID>
+int launch_hidden(const DecodeArgs &a, hipStream_t stream) {
+  switch (a.n_hidden) {
+    case 1: return launch_mip<NL, CH, HID, 1>(a, stream);
+    case 2: return launch_mip<NL, CH, HID, 2>(a, stream);
+    default: return NTC_ERR_UNSUPPORTED;
+  }
 }
 
 }  // namespace
@@ -589,15 +748,14 @@ int launch_mip(const DecodeArgs &a, hipStream_t stream) {
 int launch_decode(const DecodeArgs &a, int n_levels, int channels, int feat, int hidden,
                   hipStream_t stream) {
   (void)feat;
-  if (a.n_hidden < 0 || a.n_hidden > kMaxHidden) return NTC_ERR_UNSUPPORTED;
   if (hidden == 64) {
-    if (n_levels == 2 && channels == 8) return launch_mip<2, 8, 64>(a, stream);
-    if (n_levels == 2 && channels == 16) return launch_mip<2, 16, 64>(a, stream);
-    if (n_levels == 3 && channels == 16) return launch_mip<3, 16, 64>(a, stream);
+    if (n_levels == 2 && channels == 8) return launch_hidden<2, 8, 64>(a, stream);
+    if (n_levels == 2 && channels == 16) return launch_hidden<2, 16, 64>(a, stream);
+    if (n_levels == 3 && channels == 16) return launch_hidden<3, 16, 64>(a, stream);
   } else if (hidden == 128) {
-    if (n_levels == 2 && channels == 8) return launch_mip<2, 8, 128>(a, stream);
-    if (n_levels == 2 && channels == 16) return launch_mip<2, 16, 128>(a, stream);
-    if (n_levels == 3 && channels == 16) return launch_mip<3, 16, 128>(a, stream);
+    if (n_levels == 2 && channels == 8) return launch_hidden<2, 8, 128>(a, stream);
+    if (n_levels == 2 && channels == 16) return launch_hidden<2, 16, 128>(a, stream);
+    if (n_levels == 3 && channels == 16) return launch_hidden<3, 16, 128>(a, stream);
   }
   return NTC_ERR_UNSUPPORTED;
 }

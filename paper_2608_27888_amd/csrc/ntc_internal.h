@@ -66,7 +66,7 @@ int launch_divergence(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_
 struct DecodeArgs {
   const uint16_t *latents;
   int64_t tex_stride;                 // fp16 values per texture
-  int32_t level_off[NTC_MAX_LEVELS];  // fp16 offset of each level in a texture
+  uint32_t level_off[NTC_MAX_LEVELS]; // fp16 offset of each level in a texture
   int32_t res[NTC_MAX_LEVELS];
   float resf[NTC_MAX_LEVELS];
   int32_t n_textures;
