@@ -449,7 +449,7 @@ __device__ __forceinline__ floatx16 out_bias(const uint32_t *lds, const Image &i
   const int h = lane_id() >> 5;
   floatx16 b = {};
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
+  for (int g = 0; g < 2; ++g) {
     if (8 * g >= out_dim) break;
     const floatx4 v = *(const floatx4 *)(bl + 8 * g + 4 * h);
     b[4 * g + 0] = v[0];
@@ -470,43 +470,76 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_resource(const DecodeArgs 
                                            0x00020000);
 }
 
-// Bias, sigmoid and store of the output rows held by this lane (rows 8g + 4h + r
-// of the query in its column), as 16-byte stores; the output width is a
-// multiple of 4.  The loop bound depends on the output width only, so no lane
-// computes rows past it.
-__device__ __forceinline__ void store_out(__amdgpu_buffer_rsrc_t out, int out_dim, uint32_t q,
-                                          bool ok, const floatx16 &z, const floatx16 &bias) {
-  const int h = lane_id() >> 5;
+// Decoded values this lane stores for one 32-query column block: rows 4h..4h+3
+// (lo) and 8+4h..8+4h+3 (hi) of the query in its column, after bias and sigmoid.
+// The output width is <= 16 and a multiple of 4; hi is computed only when the
+// width reaches it.
+struct OutRows {
+  u32x4 lo, hi;
+};
+
+__device__ __forceinline__ OutRows finish_rows(const floatx16 &z, const floatx16 &bias,
+                                               int out_dim) {
+  OutRows r;
+  r.hi = u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    if (8 * g >= out_dim) break;
-    u32x4 y;
+  for (int i = 0; i < 4; ++i) r.lo[i] = __builtin_bit_cast(uint32_t, sigmoid(z[i] + bias[i]));
+  if (out_dim > 8) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      y[r] = __builtin_bit_cast(uint32_t, sigmoid(z[4 * g + r] + bias[4 * g + r]));
-    const int r0 = 8 * g + 4 * h;
-    const uint32_t off =
-        ok && r0 < out_dim ? (q * (uint32_t)out_dim + (uint32_t)r0) * 4u : kDropOffset;
-    __builtin_amdgcn_raw_buffer_store_b128(y, out, off, 0, 0);
+    for (int i = 0; i < 4; ++i)
+      r.hi[i] = __builtin_bit_cast(uint32_t, sigmoid(z[4 + i] + bias[4 + i]));
   }
+  return r;
+}
+
+// Both 16-byte stores are always issued (rows past the width, and masked
+// lanes, get the drop offset), so the number of stores never depends on the
+// data or the width.
+__device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t out, int out_dim, uint32_t q,
+                                           bool ok, const OutRows &r) {
+  const int h = lane_id() >> 5;
+  const uint32_t row = q * (uint32_t)out_dim;
+  const int r0 = 4 * h, r1 = 8 + 4 * h;
+  const uint32_t off0 = ok && r0 < out_dim ? (row + (uint32_t)r0) * 4u : kDropOffset;
+  const uint32_t off1 = ok && r1 < out_dim ? (row + (uint32_t)r1) * 4u : kDropOffset;
+  __builtin_amdgcn_raw_buffer_store_b128(r.lo, out, off0, 0, 0);
+  __builtin_amdgcn_raw_buffer_store_b128(r.hi, out, off1, 0, 0);
+}
+
+// Column block 0 holds the queries of lanes 0..31, block 1 those of lanes
+// 32..63; a lane of half h stores, for each block, the query of lane
+// (block * 32 + lane % 32): its own in block h, its partner's in the other.
+__device__ __forceinline__ void store_tile(__amdgpu_buffer_rsrc_t out, int out_dim, uint32_t q,
+                                           bool ok, const OutRows &b0, const OutRows &b1) {
+  const uint32_t q_other = (uint32_t)__shfl_xor((int)q, 32, kWave);
+  const bool ok_other = __shfl_xor((int)ok, 32, kWave) != 0;
+  const bool h = lane_id() >= 32;
+  store_rows(out, out_dim, h ? q_other : q, h ? ok_other : ok, b0);
+  store_rows(out, out_dim, h ? q : q_other, h ? ok : ok_other, b1);
 }
 
 // Query data of a slot.  The loads are unconditional (a slot without a valid
-// query reads query 0 and is marked invalid), so every wave issues the same
-// number of loads on every path and waits stay exact; the texture id is
-// checked once it has arrived.
+// query reads query 0), so every wave issues the same loads on every path and
+// the compiler's waits stay exact.  The texture id is checked by validate(),
+// once the tile that owns the query is about to use it.
 template <int NL, bool MIP>
 __device__ __forceinline__ Query load_query(const DecodeArgs &a, uint32_t q, bool in_range) {
   Query r;
   r.q = q;
-  const bool ok = in_range && q < a.n;
-  const uint32_t qs = ok ? q : 0u;
+  r.valid = in_range && q < a.n;
+  const uint32_t qs = r.valid ? q : 0u;
   r.tex = a.tex_id[qs];
   const float2 uv = ((const float2 *)a.uv)[qs];
   r.u = uv.x;
   r.v = uv.y;
   r.mip = MIP ? a.mip[qs] : 0.f;
-  r.valid = ok && r.tex < (uint32_t)a.n_textures;
+  return r;
+}
+
+// Marks a query with an out-of-range texture invalid and points it at texture
+// 0, so its (discarded) gather stays inside the latents.
+__device__ __forceinline__ Query validate(const DecodeArgs &a, Query r) {
+  r.valid = r.valid && r.tex < (uint32_t)a.n_textures;
   if (!r.valid) r.tex = 0;
   return r;
 }
@@ -561,7 +594,7 @@ decode_binned(const DecodeArgs a) {
   const uint32_t total_tiles = (uint32_t)(slots / kWave);
   const uint32_t per = (total_tiles + gridDim.x - 1) / gridDim.x;
   const uint32_t blk = xcd_local_block(blockIdx.x, gridDim.x);
-  uint32_t t = blk * per;
+  const uint32_t t = blk * per;
   const uint32_t t_end = min(t + per, total_tiles);
   if (t >= t_end) return;
   // bin holding slot 64 t: the last d with bin_offset[d] <= 64 t
@@ -571,63 +604,101 @@ decode_binned(const DecodeArgs a) {
     if (bin_off(a, mid) <= t * kWave) lo = mid; else hi = mid;
   }
   // Tiles go in groups of up to four consecutive tiles of one bin, tile t + w to
-  // wave w; every wave walks the same (uniform) sequence of groups.
+  // wave w; every wave walks the same (uniform) sequence of groups.  A wave
+  // without a tile in a group runs it with every lane masked.
   Group g0 = group_at(a, t, lo, bin_off(a, lo + 1) / kWave, D, t_end);
   Group g1 = next_group(a, g0, D, t_end);
   Group g2 = next_group(a, g1, D, t_end);
-  // perm entry of this wave's tile in group g (NTC_PAD when the wave has none);
-  // the load itself is unconditional (slot 0 exists whenever there is a tile)
-  auto slot_query = [&](const Group &g) -> uint32_t {
-    const bool has = w < g.n;
-    const uint32_t v = a.perm[has ? (g.t + w) * kWave + lane : 0u];
-    return has ? v : NTC_PAD;
+  Group g3 = next_group(a, g2, D, t_end);
+  // perm entry of this wave's tile in group g.  The load is unconditional (slot
+  // 0 exists whenever there is a tile) and the entry stays raw until it is
+  // used, with `has` saying whether the wave has a tile in the group: selecting
+  // right after the load would wait for it.
+  struct Slot {
+    uint32_t raw;
+    bool has;
   };
-  uint32_t staged = 0xFFFFFFFFu;
-  // Software pipeline, uniform across waves (a wave without a tile in a group
-  // runs it with every lane masked): while tile k is gathered and decoded, the
-  // query data of tile k+1 and the permutation entry of tile k+2 are in
-  // flight.  Loads are issued in the order they are consumed, so each wait only
-  // drains the oldest loads.
-  Query q0 = load_query<NL, MIP>(a, slot_query(g0), true);
-  uint32_t p1 = slot_query(g1);
-  while (g0.n) {
-    if (g0.d != staged) {
-      __syncthreads();
-      stage_decoder<NL, CH, HID>(a, g0.d, lds);
-      __syncthreads();
-      staged = g0.d;
-    }
+  auto slot_query = [&](const Group &g) -> Slot {
+    const bool has = w < g.n;
+    return Slot{a.perm[has ? (g.t + w) * kWave + lane : 0u], has};
+  };
+  // Software pipeline.  Vector-memory operations complete in issue order as
+  // far as the wait counter is concerned, and stores count too, so the order
+  // at the end of tile k is: taps of tile k+1, query data of tile k+2,
+  // permutation entry of tile k+3, and only then the stores of tile k.  Tile
+  // k+1 then waits for its taps without waiting for those stores, and every
+  // prefetch has a whole tile of work to land.
+  auto restage = [&](uint32_t d) {
+    __syncthreads();  // every wave is done with the previous decoder
+    stage_decoder<NL, CH, HID>(a, d, lds);
+    __syncthreads();
+  };
+  const Slot s0 = slot_query(g0);
+  Query cur = validate(a, load_query<NL, MIP>(a, s0.raw, s0.has));  // tile 0
+  restage(g0.d);
+  uint32_t staged = g0.d;
+  TileTaps<NL, CH> taps;
+  if constexpr (!MIP) fetch_taps<NL, CH>(a, cur, taps);
+  __builtin_amdgcn_sched_barrier(0);
+  const Slot s1 = slot_query(g1);
+  Query q_next = load_query<NL, MIP>(a, s1.raw, s1.has);  // tile 1
+  Slot p_next = slot_query(g2);                            // tile 2
+  __builtin_amdgcn_sched_barrier(0);
+  // As many stores as a loop iteration issues, all past the range (dropped):
+  // the loop is entered with the same operations in flight, in the same
+  // order, as at its back edge, so the waits at its top need not drain.
+  // Distinct offsets keep them from being merged.
+#pragma unroll
+  for (uint32_t i = 0; i < 4; ++i)
+    __builtin_amdgcn_raw_buffer_store_b128(u32x4{0u, 0u, 0u, 0u}, out_rsrc,
+                                           kDropOffset + 16u * i, 0, 0);
+  // One tile: decode `cur` (taps already in flight), stage the next group's
+  // decoder if it changes, fetch the next tile's taps from q_in (its query data),
+  // prefetch query data of the tile after from p_in into q_out and the
+  // permutation entry of the tile after that into p_out, then store.
+  auto tile = [&](const Query &q_in, const Slot &p_in, Query &q_out, Slot &p_out) {
     uint32_t x[S::F / 2];
-    Query q1;
-    uint32_t p2;
-    if constexpr (MIP) {
-      q1 = load_query<NL, MIP>(a, p1, true);
-      p2 = slot_query(g2);
-      gather<NL, CH, MIP>(a, q0, x);
-    } else {
-      TileTaps<NL, CH> taps;
-      fetch_taps<NL, CH>(a, q0, taps);
-      q1 = load_query<NL, MIP>(a, p1, true);
-      p2 = slot_query(g2);
-      // all loads above are issued before any of them is waited on
-      __builtin_amdgcn_sched_barrier(0);
+    if constexpr (MIP)
+      gather<NL, CH, MIP>(a, cur, x);
+    else
       interp_taps<NL, CH>(taps, x);
-    }
     half8 xb0[S::KS0], xb1[S::KS0];
     to_b_operands<S::KS0>(x, xb0, xb1);
-    floatx16 y0, y1;
-    run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, y0, y1);
-    const uint32_t q_other = (uint32_t)__shfl_xor((int)q0.q, 32, kWave);
-    const bool ok_other = __shfl_xor((int)q0.valid, 32, kWave) != 0;
-    const bool h = lane >= 32;
+    floatx16 z0, z1;
+    run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, z0, z1);
     const floatx16 ob = out_bias(lds, image_of<NL, CH, HID>(NH), HID, NH, a.out_dim);
-    store_out(out_rsrc, a.out_dim, h ? q_other : q0.q, h ? ok_other : q0.valid, y0, ob);
-    store_out(out_rsrc, a.out_dim, h ? q0.q : q_other, h ? q0.valid : ok_other, y1, ob);
-    q0 = q1;
-    p1 = p2;
+    const OutRows r0 = finish_rows(z0, ob, a.out_dim);
+    const OutRows r1 = finish_rows(z1, ob, a.out_dim);
+    __builtin_amdgcn_sched_barrier(0);
+    // The next group's decoder is staged here, between this tile's MLP and the
+    // next tile's fetches, so no fetched data is live across the staging.
+    if (g1.n && g1.d != staged) {
+      restage(g1.d);
+      staged = g1.d;
+    }
+    // next tile: taps, then the prefetches, then this tile's stores
+    const Query nxt = validate(a, q_in);
+    if constexpr (!MIP) fetch_taps<NL, CH>(a, nxt, taps);
+    __builtin_amdgcn_sched_barrier(0);
+    q_out = load_query<NL, MIP>(a, p_in.raw, p_in.has);
+    p_out = slot_query(g3);
+    __builtin_amdgcn_sched_barrier(0);
+    store_tile(out_rsrc, a.out_dim, cur.q, cur.valid, r0, r1);
+    cur = nxt;
     g0 = g1;
     g1 = g2;
-    g2 = next_group(a, g2, D, t_end);
+    g2 = g3;
+    g3 = next_group(a, g3, D, t_end);
+  };
+  // Unrolled by two with the prefetch registers swapping roles, so a fetched
+  // value is never copied between registers (a copy would wait for the fetch).
+  Query q_b;
+  Slot p_b;
+  for (;;) {
+    if (!g0.n) break;
+    tile(q_next, p_next, q_b, p_b);
+    if (!g0.n) break;
+    tile(q_b, p_b, q_next, p_next);
   }
 }
 
@@ -646,10 +717,9 @@ decode_stream(const DecodeArgs a) {
   const uint32_t g_begin = blk * per, g_end = min(g_begin + per, n_groups);
   uint32_t staged = 0xFFFFFFFFu;
   int parity = 0;
-  const bool h = lane >= 32;
   for (uint32_t g = g_begin; g < g_end; ++g) {
     const uint32_t q = (g * kWavesPerBlock + w) * kWave + lane;
-    const Query qq = load_query<NL, MIP>(a, q, true);
+    const Query qq = validate(a, load_query<NL, MIP>(a, q, true));
     uint32_t dq = 0xFFFFFFFFu;
     bool live = qq.valid;
     if (live) {
@@ -661,7 +731,6 @@ decode_stream(const DecodeArgs a) {
     gather<NL, CH, MIP>(a, qq, x);
     half8 xb0[S::KS0], xb1[S::KS0];
     to_b_operands<S::KS0>(x, xb0, xb1);
-    const uint32_t q_other = (uint32_t)__shfl_xor((int)q, 32, kWave);
     uint64_t todo = ballot(live);
     for (;;) {
       const uint32_t mine =
@@ -681,13 +750,11 @@ decode_stream(const DecodeArgs a) {
       const bool mine_now = live && dq == d;
       const uint64_t sel = ballot(mine_now);
       if (sel) {
-        floatx16 y0, y1;
-        run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, y0, y1);
-        const bool sel_other = __shfl_xor((int)mine_now, 32, kWave) != 0;
-        const floatx16 ob = out_bias(lds, image_of<NL, CH, HID>(NH), HID, NH,
-                                     a.out_dim);
-        store_out(out_rsrc, a.out_dim, h ? q_other : q, h ? sel_other : mine_now, y0, ob);
-        store_out(out_rsrc, a.out_dim, h ? q : q_other, h ? mine_now : sel_other, y1, ob);
+        floatx16 z0, z1;
+        run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, z0, z1);
+        const floatx16 ob = out_bias(lds, image_of<NL, CH, HID>(NH), HID, NH, a.out_dim);
+        store_tile(out_rsrc, a.out_dim, q, mine_now, finish_rows(z0, ob, a.out_dim),
+                   finish_rows(z1, ob, a.out_dim));
         todo &= ~sel;
         live = live && !mine_now;
       }
