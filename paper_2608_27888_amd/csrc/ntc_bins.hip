@@ -5,47 +5,46 @@
 // shared decoder creates (Sec. 1; Sec. 4.4 "Performance analysis").  The
 // binning itself is not in the paper.
 //
-// Three kernels, one pass each over the ids:
-//   hist    : workgroup b counts the decoder ids of its chunk of queries into an
-//             LDS histogram and writes it as column b of hist[d][b]; row D
-//             counts the chunk's invalid queries.
+// Three kernels:
+//   hist    : workgroup b resolves the decoder id of every query of its chunk
+//             (tex_to_dec[tex_id[q]]), stores it as a 16-bit id for the scatter,
+//             and counts the ids into an LDS histogram written as column b of
+//             hist[d][b]; row D counts the chunk's invalid queries.
 //   scan    : workgroup d turns row d into an exclusive prefix over chunks and
 //             writes bin_count[d]; the last workgroup to finish (found with a
 //             device-scope counter) scans the counts into the padded
 //             bin_offset and fills the padding slots with NTC_PAD.
-//   scatter : workgroup b walks its chunk again in order and writes each query
-//             to bin_offset[d] + hist[d][b] + (rank of the query inside the
-//             chunk among queries of decoder d).
+//   scatter : workgroup b walks its chunk again in order, reading the 16-bit
+//             ids, and writes each query to bin_offset[d] + hist[d][b] + (rank
+//             of the query inside the chunk among queries of decoder d).
 // Ranks inside a wave come from ballots over the distinct ids present (a peel
 // loop whose trip count is the number of distinct decoders in the wave), so the
 // order inside a bin is ascending query index: the permutation is unique.
+// Each thread issues a whole batch of loads before it consumes any of them.
 #include "ntc_internal.h"
 
 namespace ntc {
 namespace {
 
-constexpr int kRows = 4;                           // 64-query rows per wave per tile
-constexpr int kTile = kBlock * kRows;              // queries per workgroup step
-constexpr int64_t kMinChunk = 8 * kTile;           // queries per workgroup, at least
+constexpr int kBatch = 16;                         // ids per thread per histogram batch
+constexpr int kRows = 8;                           // 64-query rows per wave per scatter tile
+constexpr int kTile = kBlock * kRows;              // queries per scatter step of a workgroup
+constexpr int64_t kChunkQuantum = kBlock * kBatch; // chunks are multiples of this (and of kTile)
+constexpr int64_t kMinChunk = 2 * kChunkQuantum;   // queries per workgroup, at least
 constexpr int64_t kTargetBlocks = 1024;
+constexpr uint16_t kInvalid16 = 0xFFFF;            // 16-bit id of an invalid query
+constexpr int kScanPerThread = 8;                  // chunks per thread in the row scan
 
 // The workspace starts with kStatusWords status words -- [0] scan completion
-// counter, [1] invalid query count -- followed by the chunk histograms.
+// counter, [1] invalid query count -- followed by the chunk histograms and then
+// the 16-bit decoder id of every query.
 constexpr int kStatusWords = 4;
-
-__device__ __forceinline__ uint32_t decoder_of(const uint32_t *tex_id, const uint32_t *tex_to_dec,
-                                               uint32_t q, uint32_t n_textures,
-                                               uint32_t n_decoders) {
-  uint32_t t = tex_id[q];
-  uint32_t d = t < n_textures ? tex_to_dec[t] : n_decoders;
-  return d < n_decoders ? d : n_decoders;  // n_decoders marks an invalid query
-}
 
 __global__ void __launch_bounds__(kBlock)
 bins_hist(const uint32_t *__restrict__ tex_id, uint32_t n,
           const uint32_t *__restrict__ tex_to_dec, uint32_t n_textures, uint32_t n_decoders,
           uint32_t chunk, uint32_t nblocks, uint32_t *__restrict__ hist,
-          uint32_t *__restrict__ status) {
+          uint32_t *__restrict__ status, uint16_t *__restrict__ dec16) {
   extern __shared__ uint32_t lds_hist[];  // n_decoders + 1 counters
   const uint32_t b = blockIdx.x;
   for (uint32_t d = threadIdx.x; d <= n_decoders; d += kBlock) lds_hist[d] = 0;
@@ -53,21 +52,32 @@ bins_hist(const uint32_t *__restrict__ tex_id, uint32_t n,
   __syncthreads();
   const uint64_t begin = (uint64_t)b * chunk;
   const uint64_t end = begin + chunk < n ? begin + chunk : n;
-  const uint64_t iters = (end - begin + kBlock - 1) / kBlock;
-  for (uint64_t it = 0; it < iters; ++it) {
-    // every wave runs the same trip count; lanes past `end` hold no id
-    const uint64_t i = begin + it * kBlock + threadIdx.x;
-    const bool inside = i < end;
-    const uint32_t d = inside ? decoder_of(tex_id, tex_to_dec, (uint32_t)i, n_textures,
-                                           n_decoders)
-                              : 0xFFFFFFFFu;
-    uint64_t todo = ballot(inside);
-    while (todo) {
-      const uint32_t leader = (uint32_t)__builtin_ctzll(todo);
-      const uint32_t dl = read_lane(d, leader);
-      const uint64_t same = ballot(d == dl) & todo;
-      if (lane_id() == leader) atomicAdd(&lds_hist[dl], (uint32_t)__builtin_popcountll(same));
-      todo &= ~same;
+  for (uint64_t base = begin; base < end; base += kChunkQuantum) {
+    // row j of the batch: queries base + j * kBlock + thread
+    uint32_t t[kBatch], d[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const uint64_t i = base + (uint64_t)j * kBlock + threadIdx.x;
+      t[j] = i < end ? tex_id[i] : 0xFFFFFFFFu;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const uint32_t dd = t[j] < n_textures ? tex_to_dec[t[j]] : n_decoders;
+      d[j] = dd < n_decoders ? dd : n_decoders;  // n_decoders marks an invalid query
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const uint64_t i = base + (uint64_t)j * kBlock + threadIdx.x;
+      const bool inside = i < end;
+      if (inside) dec16[i] = d[j] < n_decoders ? (uint16_t)d[j] : kInvalid16;
+      uint64_t todo = ballot(inside);
+      while (todo) {
+        const uint32_t leader = (uint32_t)__builtin_ctzll(todo);
+        const uint32_t dl = read_lane(d[j], leader);
+        const uint64_t same = ballot(d[j] == dl) & todo;
+        if (lane_id() == leader) atomicAdd(&lds_hist[dl], (uint32_t)__builtin_popcountll(same));
+        todo &= ~same;
+      }
     }
   }
   __syncthreads();
@@ -105,18 +115,22 @@ bins_scan(uint32_t *__restrict__ hist, uint32_t nblocks, uint32_t n_decoders, ui
   __shared__ uint32_t lds_last;
   const uint32_t d = blockIdx.x;  // row; row n_decoders counts invalid queries
   uint32_t *row = hist + (size_t)d * nblocks;
-  // each thread owns a contiguous run of the row
-  const uint32_t per = (nblocks + kBlock - 1) / kBlock;
-  const uint32_t lo = threadIdx.x * per;
-  const uint32_t hi = lo + per < nblocks ? lo + per : nblocks;
+  // each thread owns kScanPerThread consecutive chunks of the row (nblocks is
+  // at most kBlock * kScanPerThread); all of them are loaded at once
+  const uint32_t lo = threadIdx.x * kScanPerThread;
+  uint32_t v[kScanPerThread];
   uint32_t sum = 0;
-  for (uint32_t i = lo; i < hi; ++i) sum += row[i];
+#pragma unroll
+  for (int k = 0; k < kScanPerThread; ++k) {
+    v[k] = lo + k < nblocks ? row[lo + k] : 0u;
+    sum += v[k];
+  }
   uint32_t excl;
   const uint32_t total = block_exclusive_scan(sum, excl, lds_tmp);
-  for (uint32_t i = lo; i < hi; ++i) {
-    uint32_t c = row[i];
-    row[i] = excl;
-    excl += c;
+#pragma unroll
+  for (int k = 0; k < kScanPerThread; ++k) {
+    if (lo + k < nblocks) row[lo + k] = excl;
+    excl += v[k];
   }
   if (threadIdx.x == 0) {
     if (d < n_decoders) bin_count[d] = total;
@@ -150,8 +164,7 @@ bins_scan(uint32_t *__restrict__ hist, uint32_t nblocks, uint32_t n_decoders, ui
 }
 
 __global__ void __launch_bounds__(kBlock)
-bins_scatter(const uint32_t *__restrict__ tex_id, uint32_t n,
-             const uint32_t *__restrict__ tex_to_dec, uint32_t n_textures, uint32_t n_decoders,
+bins_scatter(const uint16_t *__restrict__ dec16, uint32_t n, uint32_t n_decoders,
              uint32_t chunk, uint32_t nblocks, const uint32_t *__restrict__ hist,
              const uint32_t *__restrict__ bin_offset, uint32_t *__restrict__ perm) {
   // cursor[d]: next free slot of bin d for this chunk;
@@ -170,15 +183,24 @@ bins_scatter(const uint32_t *__restrict__ tex_id, uint32_t n,
   uint32_t *my_cnt = wave_cnt + w * n_decoders;
   const uint64_t begin = (uint64_t)b * chunk;
   const uint64_t end = begin + chunk < n ? begin + chunk : n;
-  for (uint64_t tile = begin; tile < end; tile += kTile) {
-    // wave w owns queries [tile + w*64*kRows, +64*kRows), row r lane l -> + r*64 + l
-    uint32_t dec[kRows], rank[kRows];
+  // wave w owns queries [tile + w*64*kRows, +64*kRows) of a tile; row r lane l
+  // holds query tile + w*64*kRows + r*64 + l.  The next tile's ids are fetched
+  // while the current one is ranked and scattered.
+  auto fetch = [&](uint64_t tile, uint32_t (&dec)[kRows]) {
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
       const uint64_t q = tile + (uint64_t)w * kWave * kRows + r * kWave + lane;
-      dec[r] = q < end ? decoder_of(tex_id, tex_to_dec, (uint32_t)q, n_textures, n_decoders)
-                       : n_decoders;
+      const uint16_t v = q < end ? dec16[q] : kInvalid16;
+      dec[r] = v == kInvalid16 ? n_decoders : (uint32_t)v;
     }
+  };
+  uint32_t nxt[kRows];
+  if (begin < end) fetch(begin, nxt);
+  for (uint64_t tile = begin; tile < end; tile += kTile) {
+    uint32_t dec[kRows], rank[kRows];
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) dec[r] = nxt[r];
+    if (tile + kTile < end) fetch(tile + kTile, nxt);
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
       uint64_t todo = ballot(dec[r] < n_decoders);
@@ -224,14 +246,19 @@ bins_scatter(const uint32_t *__restrict__ tex_id, uint32_t n,
 BinsLayout bins_layout(int64_t n, int32_t n_decoders) {
   BinsLayout L;
   int64_t chunk = (n + kTargetBlocks - 1) / kTargetBlocks;
-  chunk = (chunk + kTile - 1) / kTile * kTile;
+  chunk = (chunk + kChunkQuantum - 1) / kChunkQuantum * kChunkQuantum;
   if (chunk < kMinChunk) chunk = kMinChunk;
   L.chunk = chunk;
   L.blocks = n > 0 ? (n + chunk - 1) / chunk : 1;
   L.hist_words = (size_t)(n_decoders + 1) * (size_t)L.blocks;
-  L.bytes = (L.hist_words + kStatusWords) * sizeof(uint32_t);
+  const size_t dec_words = ((size_t)n + 1) / 2;  // 16-bit ids, two per word
+  L.bytes = (kStatusWords + L.hist_words + dec_words) * sizeof(uint32_t);
   return L;
 }
+
+static_assert(kChunkQuantum % kTile == 0, "scatter tiles must divide the chunks");
+static_assert(kTargetBlocks + 1 <= (int64_t)kBlock * kScanPerThread,
+              "the row scan covers every chunk");
 
 int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
                       int32_t n_textures, int32_t n_decoders, int32_t align,
@@ -240,6 +267,7 @@ int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_
   const BinsLayout L = bins_layout(n, n_decoders);
   uint32_t *status = (uint32_t *)workspace;
   uint32_t *hist = status + kStatusWords;
+  uint16_t *dec16 = (uint16_t *)(hist + L.hist_words);
   const uint32_t D = (uint32_t)n_decoders;
   const size_t lds_hist = (size_t)(D + 1) * sizeof(uint32_t);
   const size_t lds_scatter = (size_t)D * (1 + kWavesPerBlock) * sizeof(uint32_t);
@@ -251,13 +279,13 @@ int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_
   }
   hipLaunchKernelGGL(bins_hist, dim3((unsigned)L.blocks), dim3(kBlock), lds_hist, stream, tex_id,
                      (uint32_t)n, tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk,
-                     (uint32_t)L.blocks, hist, status);
+                     (uint32_t)L.blocks, hist, status, dec16);
   hipLaunchKernelGGL(bins_scan, dim3(D + 1), dim3(kBlock), 0, stream, hist, (uint32_t)L.blocks, D,
                      (uint32_t)align, bin_count, bin_offset, perm, status);
   if (n > 0)
     hipLaunchKernelGGL(bins_scatter, dim3((unsigned)L.blocks), dim3(kBlock), lds_scatter, stream,
-                       tex_id, (uint32_t)n, tex_to_dec, (uint32_t)n_textures, D,
-                       (uint32_t)L.chunk, (uint32_t)L.blocks, hist, bin_offset, perm);
+                       dec16, (uint32_t)n, D, (uint32_t)L.chunk, (uint32_t)L.blocks, hist,
+                       bin_offset, perm);
   return hip_status(hipGetLastError());
 }
 
