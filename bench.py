@@ -46,6 +46,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample", type=int, default=1 << 22,
                    help="queries of the frame the CPU oracle decodes")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="first run a plain device-to-device copy of this many MiB three times, "
+                        "so that a counter profile of this run also holds the copy's HBM bytes")
     return p.parse_args()
 
 
@@ -68,6 +71,38 @@ def unique_latent_bytes(w) -> int:
                 keys.append((tex * r + yy) * r + xx)
         total += np.unique(np.concatenate(keys)).size * c * 2
     return int(total)
+
+
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_binned_clustered4k_hbm_traffic.md")
+DECODE_SOURCES = [os.path.join(ROOT, "paper_2608_27888_amd", "csrc", f)
+                  for f in ("ntc_decode.hip", "ntc_internal.h")]
+
+
+def decode_source_hash() -> str:
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in DECODE_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def profiled_traffic(workload: str):
+    """HBM bytes per decode launch from the committed counter profile, or None when the
+    profile covers another workload or the decode sources changed since it was taken."""
+    try:
+        with open(TRAFFIC_PROFILE) as fh:
+            fields = dict(line[2:].split(":", 1) for line in fh if line.startswith("- ") and ":" in line)
+    except OSError:
+        return None
+    fields = {k.strip(): v.strip().strip("`") for k, v in fields.items()}
+    if fields.get("workload") != workload or fields.get("decode_source_sha256") != decode_source_hash():
+        return None
+    try:
+        return int(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def timed(fn, steps, warmup, torch):
@@ -105,6 +140,15 @@ def main():
     bins = ntc.alloc_bins(n, w.n_decoders, 64, dev)
     out = torch.empty((n, w.out_dim), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
+
+    if args.copy_calibration > 0:  # reference kernel of known size for HBM byte counters
+        src = torch.ones(args.copy_calibration << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copied {args.copy_calibration} MiB three times for counter calibration")
+        del src, dst
 
     # ---------------------------------------------------------------- headline
     ev = []
@@ -154,7 +198,7 @@ def main():
         roof = {"bound": "mfma", "achieved": round(decode_flops / dsec / 1e12, 1),
                 "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = None
+    roof["traffic"] = profiled_traffic(w.name)
     roof["kernel"] = "decode_binned"
     roof["algorithmic_bytes_per_launch"] = int(decode_bytes)
     roof["algorithmic_flops_per_launch"] = int(decode_flops)
