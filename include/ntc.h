@@ -122,8 +122,9 @@ int64_t ntc_bins_capacity(int64_t n, int32_t n_decoders, int32_t align);
  * align: power of two in [1, NTC_MAX_ALIGN]; 64 (one wave) for ntc_decode.
  * perm_capacity >= ntc_bins_capacity(n, n_decoders, align) (NTC_ERR_CAPACITY).
  * workspace: device buffer of >= ntc_bins_workspace_bytes(n, n_decoders) bytes,
- * owned by the caller, contents need not be initialised; it holds the
- * invalid-query count until the next call that uses it.
+ * 16-byte aligned (NTC_ERR_ARG otherwise), owned by the caller, contents need
+ * not be initialised; it holds the invalid-query count until the next call
+ * that uses it.
  * n = 0 is valid: bin_count and bin_offset become all zero.
  */
 int ntc_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,

@@ -48,6 +48,7 @@ int ntc_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec
     return NTC_ERR_ARG;
   if (!tex_to_dec || !bin_count || !bin_offset || !workspace || (n > 0 && (!tex_id || !perm)))
     return NTC_ERR_ARG;
+  if ((uintptr_t)workspace & 15) return NTC_ERR_ARG;
   const int64_t cap = ntc_bins_capacity(n, n_decoders, align);
   if (perm_capacity < cap || cap > kMaxQueries + 1) return NTC_ERR_CAPACITY;
   if (workspace_bytes < ntc_bins_workspace_bytes(n, n_decoders)) return NTC_ERR_CAPACITY;

@@ -5,84 +5,120 @@
 // shared decoder creates (Sec. 1; Sec. 4.4 "Performance analysis").  The
 // binning itself is not in the paper.
 //
-// Three kernels:
-//   hist    : workgroup b resolves the decoder id of every query of its chunk
-//             (tex_to_dec[tex_id[q]]), stores it as a 16-bit id for the scatter,
-//             and counts the ids into an LDS histogram written as column b of
-//             hist[d][b]; row D counts the chunk's invalid queries.
-//   scan    : workgroup d turns row d into an exclusive prefix over chunks and
-//             writes bin_count[d]; the last workgroup to finish (found with a
-//             device-scope counter) scans the counts into the padded
-//             bin_offset and fills the padding slots with NTC_PAD.
-//   scatter : workgroup b walks its chunk again in order, reading the 16-bit
-//             ids, and writes each query to bin_offset[d] + hist[d][b] + (rank
-//             of the query inside the chunk among queries of decoder d).
-// Ranks inside a wave come from ballots over the distinct ids present (a peel
-// loop whose trip count is the number of distinct decoders in the wave), so the
-// order inside a bin is ascending query index: the permutation is unique.
-// Each thread issues a whole batch of loads before it consumes any of them.
+// The unit of the sort is one wave's contiguous slice of the query stream
+// (slice g = workgroup * 4 + wave).  Three kernels:
+//   hist    : every wave resolves the decoder id of each query of its slice
+//             (tex_to_dec[tex_id[q]]), stores it as a 16-bit id for the
+//             scatter, and counts the ids in a wave-private LDS histogram that
+//             becomes column g of hist[d][g]; row D counts invalid queries.
+//   scan    : workgroup d turns row d into an exclusive prefix over slices and
+//             writes bin_count[d] (row D: the invalid count).
+//   scatter : every workgroup first scans bin_count into the padded bin
+//             offsets (workgroup 0 writes bin_offset, the padding slots are
+//             shared out among the workgroups); then each wave walks its slice
+//             in order with wave-private cursors bin_offset[d] + hist[d][g] and
+//             writes every query to the next slot of its bin.
+// Inside a 64-query row the lanes that share a decoder id are ranked with a
+// ballot and a lane count, so the order inside a bin is ascending query index
+// and the permutation is unique.  A row whose queries all share the decoder of
+// the previous such row (the common case for screen-coherent material maps)
+// touches no LDS: the wave keeps that decoder's count or cursor in a register.
+// Each lane issues a whole batch of loads before it consumes any of them.
 #include "ntc_internal.h"
 
 namespace ntc {
 namespace {
 
-constexpr int kBatch = 16;                         // ids per thread per histogram batch
-constexpr int kRows = 8;                           // 64-query rows per wave per scatter tile
-constexpr int kTile = kBlock * kRows;              // queries per scatter step of a workgroup
-constexpr int64_t kChunkQuantum = kBlock * kBatch; // chunks are multiples of this (and of kTile)
-constexpr int64_t kMinChunk = 2 * kChunkQuantum;   // queries per workgroup, at least
+constexpr int kRowsPerBatch = 16;                                 // rows a wave loads at once
+constexpr int64_t kWaveQuantum = (int64_t)kWave * kRowsPerBatch;  // queries per wave batch
+constexpr int64_t kChunkQuantum = kWaveQuantum * kWavesPerBlock;  // chunks are multiples of this
+constexpr int64_t kMinChunk = 2 * kChunkQuantum;                  // queries per workgroup, at least
 constexpr int64_t kTargetBlocks = 1024;
-constexpr uint16_t kInvalid16 = 0xFFFF;            // 16-bit id of an invalid query
-constexpr int kScanPerThread = 8;                  // chunks per thread in the row scan
+constexpr uint16_t kInvalid16 = 0xFFFF;                           // 16-bit id of an invalid query
+constexpr uint32_t kOutside = 0xFFFFFFFFu;                        // marks a lane past the slice
+constexpr int kScanPerThread = 16;                                // slices per thread in the row scan
 
-// The workspace starts with kStatusWords status words -- [0] scan completion
-// counter, [1] invalid query count -- followed by the chunk histograms and then
-// the 16-bit decoder id of every query.
+// The workspace starts with kStatusWords status words -- [1] is the invalid
+// query count -- followed by the slice histograms and, from a 16-byte aligned
+// offset, the 16-bit decoder id of every query.
 constexpr int kStatusWords = 4;
+
+// Decoder id of texture t: n_decoders marks an invalid query.
+__device__ __forceinline__ uint32_t decoder_of(uint32_t t, const uint32_t *tex_to_dec,
+                                               uint32_t n_textures, uint32_t n_decoders) {
+  const uint32_t d = t < n_textures ? tex_to_dec[t] : n_decoders;
+  return d < n_decoders ? d : n_decoders;
+}
+
+// Query range [beg, end) of wave w of workgroup b.
+struct Slice {
+  uint64_t beg, end;
+};
+
+__device__ __forceinline__ Slice slice_of(uint32_t b, uint32_t w, uint64_t chunk, uint64_t n) {
+  const uint64_t cbeg = (uint64_t)b * chunk;
+  const uint64_t cend = cbeg + chunk < n ? cbeg + chunk : n;
+  const uint64_t wchunk = chunk / kWavesPerBlock;
+  const uint64_t beg = cbeg + w * wchunk < cend ? cbeg + w * wchunk : cend;
+  return Slice{beg, beg + wchunk < cend ? beg + wchunk : cend};
+}
 
 __global__ void __launch_bounds__(kBlock)
 bins_hist(const uint32_t *__restrict__ tex_id, uint32_t n,
           const uint32_t *__restrict__ tex_to_dec, uint32_t n_textures, uint32_t n_decoders,
-          uint32_t chunk, uint32_t nblocks, uint32_t *__restrict__ hist,
-          uint32_t *__restrict__ status, uint16_t *__restrict__ dec16) {
-  extern __shared__ uint32_t lds_hist[];  // n_decoders + 1 counters
-  const uint32_t b = blockIdx.x;
-  for (uint32_t d = threadIdx.x; d <= n_decoders; d += kBlock) lds_hist[d] = 0;
-  if (b == 0 && threadIdx.x == 0) status[0] = 0;  // scan completion counter
+          uint32_t chunk, uint32_t n_slices, uint32_t *__restrict__ hist,
+          uint16_t *__restrict__ dec16) {
+  extern __shared__ uint32_t lds[];  // kWavesPerBlock x (n_decoders + 1) counters
+  const uint32_t b = blockIdx.x, w = threadIdx.x / kWave, lane = lane_id();
+  const uint32_t rows = n_decoders + 1;
+  for (uint32_t i = threadIdx.x; i < kWavesPerBlock * rows; i += kBlock) lds[i] = 0;
   __syncthreads();
-  const uint64_t begin = (uint64_t)b * chunk;
-  const uint64_t end = begin + chunk < n ? begin + chunk : n;
-  for (uint64_t base = begin; base < end; base += kChunkQuantum) {
-    // row j of the batch: queries base + j * kBlock + thread
-    uint32_t t[kBatch], d[kBatch];
+  uint32_t *h = lds + w * rows;
+  const Slice sl = slice_of(b, w, chunk, n);
+  // A run of whole rows with one decoder is counted in (run_d, run_n) and
+  // added to the histogram when it ends.
+  uint32_t run_d = kOutside, run_n = 0;
+  for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
+    uint32_t t[kRowsPerBatch];
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const uint64_t i = base + (uint64_t)j * kBlock + threadIdx.x;
-      t[j] = i < end ? tex_id[i] : 0xFFFFFFFFu;
+    for (int j = 0; j < kRowsPerBatch; ++j) {
+      const uint64_t q = base + (uint64_t)j * kWave + lane;
+      t[j] = q < sl.end ? tex_id[q] : kOutside;
     }
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const uint32_t dd = t[j] < n_textures ? tex_to_dec[t[j]] : n_decoders;
-      d[j] = dd < n_decoders ? dd : n_decoders;  // n_decoders marks an invalid query
-    }
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      const uint64_t i = base + (uint64_t)j * kBlock + threadIdx.x;
-      const bool inside = i < end;
-      if (inside) dec16[i] = d[j] < n_decoders ? (uint16_t)d[j] : kInvalid16;
-      uint64_t todo = ballot(inside);
-      while (todo) {
-        const uint32_t leader = (uint32_t)__builtin_ctzll(todo);
-        const uint32_t dl = read_lane(d[j], leader);
-        const uint64_t same = ballot(d[j] == dl) & todo;
-        if (lane_id() == leader) atomicAdd(&lds_hist[dl], (uint32_t)__builtin_popcountll(same));
-        todo &= ~same;
+    for (int j = 0; j < kRowsPerBatch; ++j) {
+      const uint64_t q = base + (uint64_t)j * kWave + lane;
+      const bool inside = q < sl.end;
+      const uint32_t d = inside ? decoder_of(t[j], tex_to_dec, n_textures, n_decoders) : kOutside;
+      if (inside) dec16[q] = d < n_decoders ? (uint16_t)d : kInvalid16;
+      const uint32_t v0 = __builtin_amdgcn_readfirstlane(d);
+      if (ballot(d == v0) == ~0ull) {
+        if (v0 != kOutside) {
+          if (v0 != run_d) {
+            if (run_n && lane == 0) atomicAdd(&h[run_d], run_n);
+            run_d = v0;
+            run_n = 0;
+          }
+          run_n += kWave;
+        }
+      } else {
+        uint64_t todo = ballot(inside);
+        while (todo) {
+          const uint32_t leader = (uint32_t)__builtin_ctzll(todo);
+          const uint32_t dl = read_lane(d, leader);
+          const uint64_t same = ballot(d == dl) & todo;
+          if (lane == leader) atomicAdd(&h[dl], (uint32_t)__builtin_popcountll(same));
+          todo &= ~same;
+        }
       }
     }
   }
+  if (run_n && lane == 0) atomicAdd(&h[run_d], run_n);
   __syncthreads();
-  for (uint32_t d = threadIdx.x; d <= n_decoders; d += kBlock)
-    hist[(size_t)d * nblocks + b] = lds_hist[d];
+  for (uint32_t i = threadIdx.x; i < kWavesPerBlock * rows; i += kBlock) {
+    const uint32_t ww = i / rows, d = i % rows;
+    hist[(size_t)d * n_slices + b * kWavesPerBlock + ww] = lds[i];
+  }
 }
 
 // Exclusive scan of the kBlock values held one per thread; returns the total.
@@ -108,137 +144,123 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t &excl, uint32_t *l
 }
 
 __global__ void __launch_bounds__(kBlock)
-bins_scan(uint32_t *__restrict__ hist, uint32_t nblocks, uint32_t n_decoders, uint32_t align,
-          uint32_t *__restrict__ bin_count, uint32_t *__restrict__ bin_offset,
-          uint32_t *__restrict__ perm, uint32_t *__restrict__ status) {
+bins_scan(uint32_t *__restrict__ hist, uint32_t n_slices, uint32_t n_decoders,
+          uint32_t *__restrict__ bin_count, uint32_t *__restrict__ status) {
   __shared__ uint32_t lds_tmp[kWavesPerBlock];
-  __shared__ uint32_t lds_last;
   const uint32_t d = blockIdx.x;  // row; row n_decoders counts invalid queries
-  uint32_t *row = hist + (size_t)d * nblocks;
-  // each thread owns kScanPerThread consecutive chunks of the row (nblocks is
+  uint32_t *row = hist + (size_t)d * n_slices;
+  // each thread owns kScanPerThread consecutive slices of the row (n_slices is
   // at most kBlock * kScanPerThread); all of them are loaded at once
   const uint32_t lo = threadIdx.x * kScanPerThread;
   uint32_t v[kScanPerThread];
   uint32_t sum = 0;
 #pragma unroll
   for (int k = 0; k < kScanPerThread; ++k) {
-    v[k] = lo + k < nblocks ? row[lo + k] : 0u;
+    v[k] = lo + k < n_slices ? row[lo + k] : 0u;
     sum += v[k];
   }
   uint32_t excl;
   const uint32_t total = block_exclusive_scan(sum, excl, lds_tmp);
 #pragma unroll
   for (int k = 0; k < kScanPerThread; ++k) {
-    if (lo + k < nblocks) row[lo + k] = excl;
+    if (lo + k < n_slices) row[lo + k] = excl;
     excl += v[k];
   }
   if (threadIdx.x == 0) {
     if (d < n_decoders) bin_count[d] = total;
     else status[1] = total;
   }
-  // The last row to finish turns the counts into padded offsets.
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) lds_last = atomicAdd(&status[0], 1u) == n_decoders;
-  __syncthreads();
-  if (!lds_last) return;
-  __threadfence();
-  const uint32_t dper = (n_decoders + kBlock - 1) / kBlock;
-  const uint32_t dlo = threadIdx.x * dper;
-  const uint32_t dhi = dlo + dper < n_decoders ? dlo + dper : n_decoders;
-  uint32_t psum = 0;
-  for (uint32_t k = dlo; k < dhi; ++k) {
-    uint32_t c = __hip_atomic_load(&bin_count[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    psum += (c + align - 1) & ~(align - 1);
-  }
-  uint32_t pexcl;
-  const uint32_t ptotal = block_exclusive_scan(psum, pexcl, lds_tmp);
-  for (uint32_t k = dlo; k < dhi; ++k) {
-    uint32_t c = __hip_atomic_load(&bin_count[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    bin_offset[k] = pexcl;
-    const uint32_t padded = (c + align - 1) & ~(align - 1);
-    for (uint32_t s = pexcl + c; s < pexcl + padded; ++s) perm[s] = NTC_PAD;
-    pexcl += padded;
-  }
-  if (threadIdx.x == kBlock - 1) bin_offset[n_decoders] = ptotal;
 }
 
 __global__ void __launch_bounds__(kBlock)
 bins_scatter(const uint16_t *__restrict__ dec16, uint32_t n, uint32_t n_decoders,
-             uint32_t chunk, uint32_t nblocks, const uint32_t *__restrict__ hist,
-             const uint32_t *__restrict__ bin_offset, uint32_t *__restrict__ perm) {
-  // cursor[d]: next free slot of bin d for this chunk;
-  // wave_cnt[w][d]: queries of decoder d in wave w's part of the current tile.
-  extern __shared__ uint32_t lds[];
-  uint32_t *cursor = lds;
-  uint32_t *wave_cnt = lds + n_decoders;
-  const uint32_t b = blockIdx.x;
-  const uint32_t w = threadIdx.x / kWave, lane = lane_id();
-  for (uint32_t d = threadIdx.x; d < n_decoders; d += kBlock) {
-    cursor[d] = bin_offset[d] + hist[(size_t)d * nblocks + b];
+             uint32_t align, uint32_t chunk, uint32_t n_slices,
+             const uint32_t *__restrict__ hist, const uint32_t *__restrict__ bin_count,
+             uint32_t *__restrict__ bin_offset, uint32_t *__restrict__ perm) {
+  extern __shared__ uint32_t lds[];  // kWavesPerBlock x n_decoders cursors
+  __shared__ uint32_t lds_tmp[kWavesPerBlock];
+  const uint32_t b = blockIdx.x, w = threadIdx.x / kWave, lane = lane_id();
+  const uint32_t nblocks = gridDim.x;
+  // Padded bin offsets: thread i owns decoders [dlo, dhi).
+  const uint32_t dper = (n_decoders + kBlock - 1) / kBlock;
+  const uint32_t dlo = min(threadIdx.x * dper, n_decoders);
+  const uint32_t dhi = min(dlo + dper, n_decoders);
+  uint32_t psum = 0;
+  for (uint32_t k = dlo; k < dhi; ++k) psum += (bin_count[k] + align - 1) & ~(align - 1);
+  uint32_t off;
+  const uint32_t total = block_exclusive_scan(psum, off, lds_tmp);
+  for (uint32_t k = dlo; k < dhi; ++k) {
+    const uint32_t c = bin_count[k];
+    const uint32_t padded = (c + align - 1) & ~(align - 1);
 #pragma unroll
-    for (int k = 0; k < kWavesPerBlock; ++k) wave_cnt[k * n_decoders + d] = 0;
+    for (int i = 0; i < kWavesPerBlock; ++i)
+      lds[i * n_decoders + k] = off + hist[(size_t)k * n_slices + b * kWavesPerBlock + i];
+    if (b == 0) bin_offset[k] = off;
+    if (k % nblocks == b)  // the padding slots of bin k
+      for (uint32_t s = off + c; s < off + padded; ++s) perm[s] = NTC_PAD;
+    off += padded;
   }
+  if (b == 0 && threadIdx.x == 0) bin_offset[n_decoders] = total;
   __syncthreads();
-  uint32_t *my_cnt = wave_cnt + w * n_decoders;
-  const uint64_t begin = (uint64_t)b * chunk;
-  const uint64_t end = begin + chunk < n ? begin + chunk : n;
-  // wave w owns queries [tile + w*64*kRows, +64*kRows) of a tile; row r lane l
-  // holds query tile + w*64*kRows + r*64 + l.  The next tile's ids are fetched
-  // while the current one is ranked and scattered.
-  auto fetch = [&](uint64_t tile, uint32_t (&dec)[kRows]) {
+  uint32_t *cur = lds + w * n_decoders;
+  const Slice sl = slice_of(b, w, chunk, n);
+  auto fetch = [&](uint64_t base, uint32_t (&v)[kRowsPerBatch]) {
 #pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-      const uint64_t q = tile + (uint64_t)w * kWave * kRows + r * kWave + lane;
-      const uint16_t v = q < end ? dec16[q] : kInvalid16;
-      dec[r] = v == kInvalid16 ? n_decoders : (uint32_t)v;
+    for (int j = 0; j < kRowsPerBatch; ++j) {
+      const uint64_t q = base + (uint64_t)j * kWave + lane;
+      v[j] = q < sl.end ? dec16[q] : kInvalid16;
     }
   };
-  uint32_t nxt[kRows];
-  if (begin < end) fetch(begin, nxt);
-  for (uint64_t tile = begin; tile < end; tile += kTile) {
-    uint32_t dec[kRows], rank[kRows];
+  // (cd, cc): a decoder whose cursor lives in a register while whole rows of
+  // it follow one another; cur[cd] is stale meanwhile.
+  uint32_t cd = kOutside, cc = 0;
+  uint32_t nxt[kRowsPerBatch];
+  if (sl.beg < sl.end) fetch(sl.beg, nxt);
+  for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
+    uint32_t v[kRowsPerBatch];
 #pragma unroll
-    for (int r = 0; r < kRows; ++r) dec[r] = nxt[r];
-    if (tile + kTile < end) fetch(tile + kTile, nxt);
+    for (int j = 0; j < kRowsPerBatch; ++j) v[j] = nxt[j];
+    if (base + kWaveQuantum < sl.end) fetch(base + kWaveQuantum, nxt);
 #pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-      uint64_t todo = ballot(dec[r] < n_decoders);
-      rank[r] = 0;
-      while (todo) {
-        const uint32_t leader = (uint32_t)__builtin_ctzll(todo);
-        const uint32_t dl = read_lane(dec[r], leader);
-        const uint64_t same = ballot(dec[r] == dl) & todo;
-        const uint32_t before = my_cnt[dl];  // same address in every lane
-        if (dec[r] == dl) rank[r] = before + lanes_below(same);
-        if (lane == leader) my_cnt[dl] = before + (uint32_t)__builtin_popcountll(same);
-        todo &= ~same;
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-      const uint32_t d = dec[r];
-      if (d < n_decoders) {
-        uint32_t pos = cursor[d] + rank[r];
-        for (uint32_t k = 0; k < w; ++k) pos += wave_cnt[k * n_decoders + d];
-        perm[pos] = (uint32_t)(tile + (uint64_t)w * kWave * kRows + r * kWave + lane);
-      }
-    }
-    __syncthreads();
-    // The last query of each decoder in this wave's part hands the count on to
-    // the cursor and clears the wave's counter (all lanes read before any write).
-#pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-      const uint32_t d = dec[r];
-      const uint32_t cnt = d < n_decoders ? my_cnt[d] : 0u;
-      const bool last = d < n_decoders && rank[r] + 1 == cnt;
-      if (last) {
-        atomicAdd(&cursor[d], cnt);
-        my_cnt[d] = 0;
+    for (int j = 0; j < kRowsPerBatch; ++j) {
+      const uint32_t q = (uint32_t)(base + (uint64_t)j * kWave + lane);
+      const uint32_t d = v[j] == kInvalid16 ? n_decoders : v[j];  // lanes past the end: invalid
+      const uint32_t v0 = __builtin_amdgcn_readfirstlane(d);
+      if (ballot(d == v0) == ~0ull && v0 < n_decoders) {
+        if (v0 != cd) {
+          if (cd != kOutside && lane == 0) cur[cd] = cc;
+          cd = v0;
+          cc = cur[v0];
+        }
+        perm[cc + lane] = q;
+        cc += kWave;
+      } else {
+        if (cd != kOutside) {
+          if (lane == 0) cur[cd] = cc;
+          cd = kOutside;
+        }
+        uint64_t todo = ballot(d < n_decoders);
+        while (todo) {
+          const uint32_t leader = (uint32_t)__builtin_ctzll(todo);
+          const uint32_t dl = read_lane(d, leader);
+          const uint64_t same = ballot(d == dl) & todo;
+          const uint32_t at = cur[dl];  // same address in every lane
+          if (d == dl) perm[at + lanes_below(same)] = q;
+          if (lane == leader) cur[dl] = at + (uint32_t)__builtin_popcountll(same);
+          todo &= ~same;
+        }
       }
     }
   }
+}
+
+// Lets a kernel use more than the default 64 KB of dynamic LDS.
+int allow_lds(const void *kernel, size_t bytes) {
+  if (bytes + 64 <= 64 * 1024) return NTC_OK;
+  return hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) ==
+                 hipSuccess
+             ? NTC_OK
+             : NTC_ERR_HIP;
 }
 
 }  // namespace
@@ -250,15 +272,14 @@ BinsLayout bins_layout(int64_t n, int32_t n_decoders) {
   if (chunk < kMinChunk) chunk = kMinChunk;
   L.chunk = chunk;
   L.blocks = n > 0 ? (n + chunk - 1) / chunk : 1;
-  L.hist_words = (size_t)(n_decoders + 1) * (size_t)L.blocks;
-  const size_t dec_words = ((size_t)n + 1) / 2;  // 16-bit ids, two per word
-  L.bytes = (kStatusWords + L.hist_words + dec_words) * sizeof(uint32_t);
+  L.hist_words = (size_t)(n_decoders + 1) * (size_t)L.blocks * kWavesPerBlock;
+  L.dec_offset = ((kStatusWords + L.hist_words) * sizeof(uint32_t) + 15) & ~(size_t)15;
+  L.bytes = L.dec_offset + (((size_t)n * sizeof(uint16_t) + 15) & ~(size_t)15);
   return L;
 }
 
-static_assert(kChunkQuantum % kTile == 0, "scatter tiles must divide the chunks");
-static_assert(kTargetBlocks + 1 <= (int64_t)kBlock * kScanPerThread,
-              "the row scan covers every chunk");
+static_assert(kTargetBlocks * kWavesPerBlock <= (int64_t)kBlock * kScanPerThread,
+              "the row scan covers every slice");
 
 int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
                       int32_t n_textures, int32_t n_decoders, int32_t align,
@@ -267,25 +288,22 @@ int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_
   const BinsLayout L = bins_layout(n, n_decoders);
   uint32_t *status = (uint32_t *)workspace;
   uint32_t *hist = status + kStatusWords;
-  uint16_t *dec16 = (uint16_t *)(hist + L.hist_words);
+  uint16_t *dec16 = (uint16_t *)((char *)workspace + L.dec_offset);
   const uint32_t D = (uint32_t)n_decoders;
-  const size_t lds_hist = (size_t)(D + 1) * sizeof(uint32_t);
-  const size_t lds_scatter = (size_t)D * (1 + kWavesPerBlock) * sizeof(uint32_t);
-  if (lds_scatter > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void *)bins_scatter,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)lds_scatter);
-    if (e != hipSuccess) return NTC_ERR_HIP;
-  }
+  const uint32_t n_slices = (uint32_t)L.blocks * kWavesPerBlock;
+  const size_t lds_hist = (size_t)kWavesPerBlock * (D + 1) * sizeof(uint32_t);
+  const size_t lds_scatter = (size_t)kWavesPerBlock * D * sizeof(uint32_t);
+  int st = allow_lds((const void *)bins_hist, lds_hist);
+  if (st == NTC_OK) st = allow_lds((const void *)bins_scatter, lds_scatter);
+  if (st != NTC_OK) return st;
   hipLaunchKernelGGL(bins_hist, dim3((unsigned)L.blocks), dim3(kBlock), lds_hist, stream, tex_id,
-                     (uint32_t)n, tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk,
-                     (uint32_t)L.blocks, hist, status, dec16);
-  hipLaunchKernelGGL(bins_scan, dim3(D + 1), dim3(kBlock), 0, stream, hist, (uint32_t)L.blocks, D,
-                     (uint32_t)align, bin_count, bin_offset, perm, status);
-  if (n > 0)
-    hipLaunchKernelGGL(bins_scatter, dim3((unsigned)L.blocks), dim3(kBlock), lds_scatter, stream,
-                       dec16, (uint32_t)n, D, (uint32_t)L.chunk, (uint32_t)L.blocks, hist,
-                       bin_offset, perm);
+                     (uint32_t)n, tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, n_slices,
+                     hist, dec16);
+  hipLaunchKernelGGL(bins_scan, dim3(D + 1), dim3(kBlock), 0, stream, hist, n_slices, D,
+                     bin_count, status);
+  hipLaunchKernelGGL(bins_scatter, dim3((unsigned)L.blocks), dim3(kBlock), lds_scatter, stream,
+                     dec16, (uint32_t)n, D, (uint32_t)align, (uint32_t)L.chunk, n_slices, hist,
+                     bin_count, bin_offset, perm);
   return hip_status(hipGetLastError());
 }
 

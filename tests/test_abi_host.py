@@ -73,6 +73,7 @@ def test_build_bins_validation(L):
     assert _bins(L, cap=100 + 2 * 63 - 1) == ntc.NTC_ERR_CAPACITY
     assert _bins(L, wsb=8) == ntc.NTC_ERR_CAPACITY
     assert _bins(L, n=1 << 32) == ntc.NTC_ERR_ARG
+    assert _bins(L, ws=ctypes.c_void_p(0x100000 + 8)) == ntc.NTC_ERR_ARG  # not 16-byte aligned
 
 
 def _decode(L, res=(256, 128), ch=(16, 16), dims=(32, 64, 64, 8), n=100, D=4, binned=False,

@@ -77,7 +77,8 @@ def test_bins_invalid_ids_and_alignments(dev, oracle, align):
     assert bad > 0 and ntc.device_error(bins) == bad
 
 
-@pytest.mark.parametrize("n", [0, 1, 63, 64, 65, 8191, 8192, 8193])
+@pytest.mark.parametrize("n", [0, 1, 3, 63, 64, 65, 2047, 2049, 4097, 8191, 8192, 8193,
+                               16385, 100003])
 def test_bins_edge_sizes(dev, oracle, n):
     rng = np.random.default_rng(n)
     T, D = 9, 5
@@ -87,6 +88,23 @@ def test_bins_edge_sizes(dev, oracle, n):
     tex_d = torch.from_numpy(tex.view(np.int32)).to(dev) if n else torch.zeros(0, dtype=torch.int32, device=dev)
     bins = ntc.build_bins(tex_d, torch.from_numpy(t2d.view(np.int32)).to(dev), D)
     cnt, off, perm, _ = oracle.build_bins(tex, t2d, D, 64)
+    assert np.array_equal(u32(bins.bin_count), cnt)
+    assert np.array_equal(u32(bins.bin_offset), off)
+    assert np.array_equal(u32(bins.perm)[: off[-1]], perm)
+
+
+@pytest.mark.parametrize("shift", [1, 2, 3])
+def test_bins_unaligned_ids(dev, oracle, shift):
+    """tex_id that does not start on a 16-byte boundary (a slice of a larger array)."""
+    rng = np.random.default_rng(shift)
+    T, D, n = 23, 7, 50021
+    t2d = rng.integers(0, D, T).astype(np.uint32)
+    tex = rng.integers(0, T, n + shift).astype(np.uint32)
+    say(f"[bins-unaligned] shift={shift}")
+    tex_d = torch.from_numpy(tex.view(np.int32)).to(dev)[shift:]
+    assert tex_d.data_ptr() % 16 != 0
+    bins = ntc.build_bins(tex_d, torch.from_numpy(t2d.view(np.int32)).to(dev), D)
+    cnt, off, perm, _ = oracle.build_bins(tex[shift:], t2d, D, 64)
     assert np.array_equal(u32(bins.bin_count), cnt)
     assert np.array_equal(u32(bins.bin_offset), off)
     assert np.array_equal(u32(bins.perm)[: off[-1]], perm)
