@@ -214,10 +214,11 @@ __device__ __forceinline__ void fetch_level(const uint16_t *tex, uint32_t level_
                                             float resf, float u, float v, LevelTaps<CH> &L) {
   const float x = __builtin_fmaf(u, resf, -0.5f), y = __builtin_fmaf(v, resf, -0.5f);
   const float hi = resf - 2.f;
-  const float x0 = __builtin_fminf(__builtin_fmaxf(__builtin_floorf(x), 0.f), hi);
-  const float y0 = __builtin_fminf(__builtin_fmaxf(__builtin_floorf(y), 0.f), hi);
-  L.fx = __builtin_fminf(__builtin_fmaxf(x - x0, 0.f), 1.f);
-  L.fy = __builtin_fminf(__builtin_fmaxf(y - y0, 0.f), 1.f);
+  // med3 clamps (a NaN coordinate converts to index 0 below)
+  const float x0 = __builtin_amdgcn_fmed3f(__builtin_floorf(x), 0.f, hi);
+  const float y0 = __builtin_amdgcn_fmed3f(__builtin_floorf(y), 0.f, hi);
+  L.fx = __builtin_amdgcn_fmed3f(x - x0, 0.f, 1.f);
+  L.fy = __builtin_amdgcn_fmed3f(y - y0, 0.f, 1.f);
   const uint32_t idx = level_off + ((uint32_t)y0 * (uint32_t)res + (uint32_t)x0) * CH;
   const u32x4 *r0 = (const u32x4 *)(tex + idx);
   const u32x4 *r1 = (const u32x4 *)(tex + idx + (uint32_t)res * CH);
@@ -245,6 +246,33 @@ __device__ __forceinline__ void interp_level(const LevelTaps<CH> &L, float *f) {
       s = __builtin_fmaf(w01, (float)c[e], s);
       s = __builtin_fmaf(w11, (float)d[e], s);
       f[8 * i + e] = s;
+    }
+  }
+}
+
+// The same bilinear weights applied in packed fp16: each operation handles a
+// channel pair, the four weights are rounded to fp16 and every product and sum
+// is an fp16 operation (one v_pk_mul_f16 and three v_pk_fma_f16 per pair).
+// This halves the interpolation's instructions; its rounding stays well inside
+// the decode tolerance.  Writes CH / 2 packed pairs, channel order.
+__device__ __forceinline__ half2v as_h2(uint32_t v) { return __builtin_bit_cast(half2v, v); }
+
+template <int CH>
+__device__ __forceinline__ void interp_level_h2(const LevelTaps<CH> &L, uint32_t *xo) {
+  const float gx = 1.f - L.fx, gy = 1.f - L.fy;
+  const float2v w0 = {gx * gy, L.fx * gy}, w1 = {gx * L.fy, L.fx * L.fy};
+  const half2v h0 = __builtin_convertvector(w0, half2v), h1 = __builtin_convertvector(w1, half2v);
+  const half2v w00 = {h0[0], h0[0]}, w10 = {h0[1], h0[1]};
+  const half2v w01 = {h1[0], h1[0]}, w11 = {h1[1], h1[1]};
+#pragma unroll
+  for (int i = 0; i < LevelTaps<CH>::NV; ++i) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      half2v r = as_h2(L.t00[i][e]) * w00;
+      r = __builtin_elementwise_fma(as_h2(L.t10[i][e]), w10, r);
+      r = __builtin_elementwise_fma(as_h2(L.t01[i][e]), w01, r);
+      r = __builtin_elementwise_fma(as_h2(L.t11[i][e]), w11, r);
+      xo[4 * i + e] = __builtin_bit_cast(uint32_t, r);
     }
   }
 }
@@ -280,10 +308,12 @@ __device__ __forceinline__ void gather(const DecodeArgs &a, const Query &qq,
   const uint16_t *tex = a.latents + (size_t)qq.tex * (size_t)a.tex_stride;
 #pragma unroll
   for (int l = 0; l < NL; ++l) {
-    float f[CH];
     if (!MIP) {
-      sample_level<CH>(tex, a.level_off[l], a.res[l], a.resf[l], qq.u, qq.v, f);
+      LevelTaps<CH> L;
+      fetch_level<CH>(tex, a.level_off[l], a.res[l], a.resf[l], qq.u, qq.v, L);
+      interp_level_h2<CH>(L, x + l * CH / 2);
     } else {
+      float f[CH];
       float m = __builtin_fminf(__builtin_fmaxf(qq.mip, 0.f), (float)(NL - 1));
       const float lod = __builtin_fmaxf((float)l, m);
       const int k0 = (int)__builtin_floorf(lod);
@@ -298,9 +328,9 @@ __device__ __forceinline__ void gather(const DecodeArgs &a, const Query &qq,
 #pragma unroll
         for (int c = 0; c < CH; ++c) f[c] = __builtin_fmaf(t, g[c] - f[c], f[c]);
       }
-    }
 #pragma unroll
-    for (int c = 0; c < CH; c += 2) x[(l * CH + c) / 2] = pack_half2(f[c], f[c + 1]);
+      for (int c = 0; c < CH; c += 2) x[(l * CH + c) / 2] = pack_half2(f[c], f[c + 1]);
+    }
   }
 }
 
@@ -323,12 +353,7 @@ template <int NL, int CH>
 __device__ __forceinline__ void interp_taps(const TileTaps<NL, CH> &T,
                                             uint32_t (&x)[NL * CH / 2]) {
 #pragma unroll
-  for (int l = 0; l < NL; ++l) {
-    float f[CH];
-    interp_level<CH>(T.lv[l], f);
-#pragma unroll
-    for (int c = 0; c < CH; c += 2) x[(l * CH + c) / 2] = pack_half2(f[c], f[c + 1]);
-  }
+  for (int l = 0; l < NL; ++l) interp_level_h2<CH>(T.lv[l], x + l * CH / 2);
 }
 
 // Exchange halves between lane l and lane l ^ 32 so that, per 16-wide K-slice,
@@ -428,9 +453,8 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
     frag += S::MB * S::KSH;
     bl += HID;
   }
-  // output layer: HID -> out (rows padded to 32); the accumulator starts at
-  // zero and the bias of the rows this lane keeps is added by the epilogue
-  floatx16 c0 = {}, c1 = {};
+  // output layer: HID -> out (rows padded to 32 with zero weights and biases)
+  floatx16 c0 = bias_frag(bl, 0), c1 = c0;
 #pragma unroll
   for (int s = 0; s < S::KSH; ++s) {
     const half8 w = a_frag(lds, frag + s);
@@ -439,25 +463,6 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
   }
   y0 = c0;
   y1 = c1;
-}
-
-// Bias of the output rows 8g + 4h + r this lane holds, for the groups g the
-// output width reaches.
-__device__ __forceinline__ floatx16 out_bias(const uint32_t *lds, const Image &im, int hid,
-                                             int n_hidden, int out_dim) {
-  const float *bl = (const float *)lds + im.bias_off + hid * (1 + n_hidden);
-  const int h = lane_id() >> 5;
-  floatx16 b = {};
-#pragma unroll
-  for (int g = 0; g < 2; ++g) {
-    if (8 * g >= out_dim) break;
-    const floatx4 v = *(const floatx4 *)(bl + 8 * g + 4 * h);
-    b[4 * g + 0] = v[0];
-    b[4 * g + 1] = v[1];
-    b[4 * g + 2] = v[2];
-    b[4 * g + 3] = v[3];
-  }
-  return b;
 }
 
 // Raw buffer resource over the output rows: a store whose byte offset lies past
@@ -471,23 +476,21 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_resource(const DecodeArgs 
 }
 
 // Decoded values this lane stores for one 32-query column block: rows 4h..4h+3
-// (lo) and 8+4h..8+4h+3 (hi) of the query in its column, after bias and sigmoid.
+// (lo) and 8+4h..8+4h+3 (hi) of the query in its column, after the sigmoid.
 // The output width is <= 16 and a multiple of 4; hi is computed only when the
-// width reaches it.
+// width reaches it (otherwise its store is dropped and its value is unused).
 struct OutRows {
   u32x4 lo, hi;
 };
 
-__device__ __forceinline__ OutRows finish_rows(const floatx16 &z, const floatx16 &bias,
-                                               int out_dim) {
+__device__ __forceinline__ OutRows finish_rows(const floatx16 &z, int out_dim) {
   OutRows r;
-  r.hi = u32x4{0u, 0u, 0u, 0u};
+  r.hi = __builtin_nondeterministic_value(r.hi);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) r.lo[i] = __builtin_bit_cast(uint32_t, sigmoid(z[i] + bias[i]));
+  for (int i = 0; i < 4; ++i) r.lo[i] = __builtin_bit_cast(uint32_t, sigmoid(z[i]));
   if (out_dim > 8) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      r.hi[i] = __builtin_bit_cast(uint32_t, sigmoid(z[4 + i] + bias[4 + i]));
+    for (int i = 0; i < 4; ++i) r.hi[i] = __builtin_bit_cast(uint32_t, sigmoid(z[4 + i]));
   }
   return r;
 }
@@ -666,9 +669,8 @@ decode_binned(const DecodeArgs a) {
     to_b_operands<S::KS0>(x, xb0, xb1);
     floatx16 z0, z1;
     run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, z0, z1);
-    const floatx16 ob = out_bias(lds, image_of<NL, CH, HID>(NH), HID, NH, a.out_dim);
-    const OutRows r0 = finish_rows(z0, ob, a.out_dim);
-    const OutRows r1 = finish_rows(z1, ob, a.out_dim);
+    const OutRows r0 = finish_rows(z0, a.out_dim);
+    const OutRows r1 = finish_rows(z1, a.out_dim);
     __builtin_amdgcn_sched_barrier(0);
     // The next group's decoder is staged here, between this tile's MLP and the
     // next tile's fetches, so no fetched data is live across the staging.
@@ -752,9 +754,8 @@ decode_stream(const DecodeArgs a) {
       if (sel) {
         floatx16 z0, z1;
         run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, z0, z1);
-        const floatx16 ob = out_bias(lds, image_of<NL, CH, HID>(NH), HID, NH, a.out_dim);
-        store_tile(out_rsrc, a.out_dim, q, mine_now, finish_rows(z0, ob, a.out_dim),
-                   finish_rows(z1, ob, a.out_dim));
+        store_tile(out_rsrc, a.out_dim, q, mine_now, finish_rows(z0, a.out_dim),
+                   finish_rows(z1, a.out_dim));
         todo &= ~sel;
         live = live && !mine_now;
       }
