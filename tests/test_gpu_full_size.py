@@ -1,0 +1,121 @@
+"""GPU parity at the full configuration sizes, in the launch configuration bench.py times.
+
+Binning, permutation and divergence counts are compared bit for bit with the
+oracle over the whole frame (the oracle's counting sort and window counts are
+cheap); decoded channels are compared on an evenly spaced sample of queries plus
+both ends of the frame, which the oracle decodes one by one in float64.  Every
+output row must be finite and in [0, 1], and the stream-order decode must equal
+the binned decode bit for bit on the whole frame.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_27888_amd import ntc
+from paper_2608_27888_amd import workloads as W
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+TOL = 2e-3
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    ntc.lib()
+    return torch.device("cuda:0")
+
+
+def u32(t):
+    return t.cpu().numpy().view(np.uint32)
+
+
+def sample(n, k):
+    s = np.unique(np.linspace(0, n - 1, k).round().astype(np.int64))
+    return np.unique(np.concatenate([s, np.arange(min(n, 97)), np.arange(max(0, n - 97), n)]))
+
+
+def check_frame(dev, oracle, w, n_sample, check_stream=True):
+    say(f"[full] {w.name}: n={w.n} T={w.n_textures} D={w.n_decoders} dims={w.dims} "
+        f"mip={w.mip is not None}")
+    model, q = ntc.upload(w, dev)
+    bins = ntc.alloc_bins(w.n, w.n_decoders, 64, dev)
+    ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders, bins=bins)
+    out = torch.empty((w.n, w.out_dim), dtype=torch.float32, device=dev)
+    ntc.decode(model, q, bins, out=out)
+    torch.cuda.synchronize()
+    say("    bins vs oracle")
+    cnt, off, perm, bad = oracle.build_bins(w.tex_id, w.tex_to_dec, w.n_decoders, 64)
+    assert np.array_equal(u32(bins.bin_count), cnt)
+    assert np.array_equal(u32(bins.bin_offset), off)
+    P = int(off[-1])
+    assert np.array_equal(u32(bins.perm)[:P], perm)
+    assert ntc.device_error(bins) == bad == 0
+    say("    divergence vs oracle")
+    per, tot = ntc.divergence_stats(q.tex_id, model.tex_to_dec, w.n_decoders)
+    per_o, tot_o = oracle.divergence(w.tex_id, w.tex_to_dec, w.n_decoders)
+    assert np.array_equal(u32(per), per_o)
+    assert np.array_equal(tot.cpu().numpy().astype(np.uint64), tot_o)
+    per_b, tot_b = ntc.divergence_stats(q.tex_id, model.tex_to_dec, w.n_decoders,
+                                        order=bins.perm[:P])
+    assert int(tot_b[3]) == 1
+    y = out.cpu().numpy()
+    assert np.all(np.isfinite(y)) and np.all((y >= 0) & (y <= 1))
+    sub = sample(w.n, n_sample)
+    say(f"    decode vs oracle on {sub.size} queries")
+    ref = oracle.decode(w, subset=sub)
+    err = np.abs(y[sub].astype(np.float64) - ref).max()
+    say(f"    max abs err {err:.3e}")
+    assert err <= TOL
+    if check_stream:
+        say("    stream order vs binned")
+        out_s = ntc.decode(model, q)
+        assert torch.equal(out_s.view(torch.int32), out.view(torch.int32))
+    del model, q, bins, out
+    torch.cuda.empty_cache()
+
+
+def test_full_tiny(dev, oracle):
+    check_frame(dev, oracle, W.tiny(), 65536)
+
+
+def test_full_single(dev, oracle):
+    check_frame(dev, oracle, W.single(), 32768)
+
+
+def test_full_divergent(dev, oracle):
+    check_frame(dev, oracle, W.divergent(), 32768)
+
+
+@pytest.fixture(scope="module")
+def clustered(dev):
+    return W.clustered4k()
+
+
+def test_full_clustered4k_d16(dev, oracle, clustered):
+    check_frame(dev, oracle, clustered, 32768)
+
+
+def test_full_clustered4k_d512(dev, oracle, clustered):
+    w = clustered.with_decoders(512, np.arange(512, dtype=np.uint32))
+    check_frame(dev, oracle, w, 32768)
+
+
+@pytest.fixture(scope="module")
+def wide(dev):
+    return W.wide_trilinear()
+
+
+def test_full_wide_trilinear_d8(dev, oracle, wide):
+    check_frame(dev, oracle, wide, 8192)
+
+
+def test_full_wide_trilinear_d512(dev, oracle, wide):
+    w = wide.with_decoders(512, np.arange(512, dtype=np.uint32))
+    check_frame(dev, oracle, w, 8192, check_stream=False)
