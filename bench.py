@@ -74,8 +74,7 @@ def unique_latent_bytes(w) -> int:
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_binned_clustered4k_hbm_traffic.md")
-DECODE_SOURCES = [os.path.join(ROOT, "paper_2608_27888_amd", "csrc", f)
-                  for f in ("ntc_decode.hip", "ntc_internal.h")]
+DECODE_SOURCES = [os.path.join(ROOT, "paper_2608_27888_amd", "csrc", "ntc_decode.hip")]
 
 
 def decode_source_hash() -> str:
@@ -241,6 +240,21 @@ def main():
                                    "divergence_metric_stream": round(divergence_metric(tot_s), 4),
                                    "divergence_metric_binned": round(divergence_metric(tot_b), 4)},
     }
+
+    # ---------------------------------------------------------------- divergence map (Sec. 2)
+    if w.screen is not None:
+        W_, H_, spp = w.screen
+        ident = torch.arange(w.n_textures, dtype=torch.int32, device=dev)
+        maps = {}
+        for tag, t2d, D in ((f"d{w.n_decoders}", model.tex_to_dec, w.n_decoders),
+                            (f"d{w.n_textures}_per_texture", ident, w.n_textures)):
+            _, hist, tot = ntc.divergence_map(q.tex_id, W_, H_, t2d, D, spp=spp, block_w=8,
+                                              block_h=8, hist_len=17)
+            tot = tot.cpu().tolist()
+            maps[tag] = {"metric": round(divergence_metric(tot), 4),
+                         "divergent_blocks_pct": round(100.0 * tot[2] / max(tot[0], 1), 2),
+                         "max": int(tot[3]), "histogram": hist.cpu().tolist()}
+        result["divergence_map_8x8"] = maps
 
     # ---------------------------------------------------------------- 2x2 comparison
     if not args.no_compare and w.name.startswith(("clustered4k", "wide_trilinear")):

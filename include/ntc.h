@@ -15,7 +15,8 @@
  *     so that every 64-lane wave of ntc_decode runs exactly one decoder;
  *   - ntc_divergence_stats counts distinct decoders per wave-sized block, the
  *     divergence map of Sec. 2, and the totals behind the metric of
- *     Eq. (normalized_ones_metric).
+ *     Eq. (normalized_ones_metric); ntc_divergence_map does the same over 2-D
+ *     screen blocks and adds the histogram of the map.
  *
  * Conventions for every entry point:
  *   - Pointers are DEVICE pointers unless marked (host).  The caller owns every
@@ -184,6 +185,29 @@ int ntc_divergence_stats(const uint32_t *tex_id, int64_t n, const uint32_t *tex_
                          int32_t n_textures, int32_t n_decoders, const uint32_t *order,
                          int64_t len, int32_t wave, uint32_t *per_wave_distinct,
                          uint64_t *totals, void *stream);
+
+/*
+ * Divergence map of Sec. 2 over screen blocks.  The queries form a screen of
+ * width x height pixels with spp samples per pixel in row-major order,
+ * q = (y * width + x) * spp + s, n = width * height * spp.  Block (i, j) holds
+ * every sample of the pixels x in [j * block_w, min(width, (j + 1) * block_w)),
+ * y in [i * block_h, min(height, (i + 1) * block_h)), so edge blocks may be
+ * partial.  map[i * Wb + j] = number of distinct decoder ids d(q) among the
+ * block's queries, skipping queries with tex_id >= n_textures or
+ * d(q) >= n_decoders; Wb = ceil(width / block_w), Hb = ceil(height / block_h);
+ * map: u32 [Hb * Wb].  histogram (u32 [hist_len]): histogram[k] = number of
+ * blocks whose count is k for k < hist_len - 1; the last entry counts every
+ * block whose count is >= hist_len - 1.  totals (u64 [4]) = {blocks with at
+ * least one query kept, sum of map, blocks with more than one decoder, largest
+ * count}; the metric of Eq. (normalized_ones_metric) over the kept blocks is
+ * totals[1] / totals[0] - 1.  Pass an identity tex_to_dec to count textures.
+ * Limits: width, height, block_w, block_h >= 1; spp 1 .. 64;
+ * width * height * spp <= 2^32 - 2; hist_len 1 .. 4096.
+ */
+int ntc_divergence_map(const uint32_t *tex_id, int32_t width, int32_t height, int32_t spp,
+                       const uint32_t *tex_to_dec, int32_t n_textures, int32_t n_decoders,
+                       int32_t block_w, int32_t block_h, uint32_t *map, uint32_t *histogram,
+                       int32_t hist_len, uint64_t *totals, void *stream);
 
 /* (host) Static description of a status code. */
 const char *ntc_status_string(int status);

@@ -131,6 +131,51 @@ int ntc_oracle_divergence(const uint32_t *tex_id, int64_t n, const uint32_t *tex
   return NTC_ORACLE_OK;
 }
 
+int ntc_oracle_divergence_map(const uint32_t *tex_id, int32_t width, int32_t height, int32_t spp,
+                              const uint32_t *tex_to_dec, int32_t n_textures, int32_t n_decoders,
+                              int32_t block_w, int32_t block_h, uint32_t *map,
+                              uint32_t *histogram, int32_t hist_len, uint64_t *totals) {
+  if (!tex_id || !tex_to_dec || !map || !histogram || !totals || width < 1 || height < 1 ||
+      spp < 1 || block_w < 1 || block_h < 1 || n_textures < 1 || n_decoders < 1 || hist_len < 1)
+    return NTC_ORACLE_ERR_ARG;
+  const int64_t bx = (width + block_w - 1) / block_w, by = (height + block_h - 1) / block_h;
+  totals[0] = totals[1] = totals[2] = totals[3] = 0;
+  for (int k = 0; k < hist_len; ++k) histogram[k] = 0;
+  const int64_t cap = (int64_t)block_w * block_h * spp;
+  uint32_t *seen = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)cap);
+  if (!seen) return NTC_ORACLE_ERR_ARG;
+  for (int64_t i = 0; i < by; ++i) {
+    for (int64_t j = 0; j < bx; ++j) {
+      /* the distinct decoder ids of block (i, j), kept as a plain list */
+      int64_t n_seen = 0;
+      for (int64_t y = i * block_h; y < height && y < (i + 1) * block_h; ++y) {
+        for (int64_t x = j * block_w; x < width && x < (j + 1) * block_w; ++x) {
+          for (int64_t s = 0; s < spp; ++s) {
+            uint32_t t = tex_id[(y * width + x) * spp + s];
+            if (t >= (uint32_t)n_textures) continue;
+            uint32_t d = tex_to_dec[t];
+            if (d >= (uint32_t)n_decoders) continue;
+            int found = 0;
+            for (int64_t k = 0; k < n_seen; ++k)
+              if (seen[k] == d) { found = 1; break; }
+            if (!found) seen[n_seen++] = d;
+          }
+        }
+      }
+      map[i * bx + j] = (uint32_t)n_seen;
+      histogram[n_seen < hist_len - 1 ? n_seen : hist_len - 1] += 1;
+      if (n_seen > 0) {
+        totals[0] += 1;
+        totals[1] += (uint64_t)n_seen;
+        if (n_seen > 1) totals[2] += 1;
+        if ((uint64_t)n_seen > totals[3]) totals[3] = (uint64_t)n_seen;
+      }
+    }
+  }
+  free(seen);
+  return NTC_ORACLE_OK;
+}
+
 /* ----------------------------------------------------------------- sampling */
 
 static double lerp(double a, double b, double t) { return a + t * (b - a); }

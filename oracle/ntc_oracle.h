@@ -74,6 +74,24 @@ int ntc_oracle_divergence(const uint32_t *tex_id, int64_t n, const uint32_t *tex
                           int64_t len, int32_t wave, uint32_t *per_wave, uint64_t *totals);
 
 /*
+ * Divergence map over screen blocks (Sec. 2: D(i,j) = number of distinct ids
+ * in block (i,j); Eq. (normalized_ones_metric) from the totals).
+ *   The queries form a width x height screen with spp samples per pixel,
+ *   q = (y * width + x) * spp + s.  Block (i, j) = pixels x in
+ *   [j*block_w, min(width, (j+1)*block_w)), y in [i*block_h, min(height,
+ *   (i+1)*block_h)), all their samples.  map[i * Wb + j] = distinct decoder ids
+ *   among the block's queries (skipping tex_id >= n_textures and decoder ids
+ *   >= n_decoders), Wb = ceil(width / block_w).
+ *   histogram[k] = blocks with count k (k < hist_len - 1); histogram[hist_len-1]
+ *   = blocks with count >= hist_len - 1.
+ *   totals as for ntc_oracle_divergence, over blocks.
+ */
+int ntc_oracle_divergence_map(const uint32_t *tex_id, int32_t width, int32_t height, int32_t spp,
+                              const uint32_t *tex_to_dec, int32_t n_textures, int32_t n_decoders,
+                              int32_t block_w, int32_t block_h, uint32_t *map,
+                              uint32_t *histogram, int32_t hist_len, uint64_t *totals);
+
+/*
  * Feature vector of each query: per slot l = 0..n_levels-1 the latent sampled
  * at uv (bilinear, texel centres at (i + 1/2)/res, clamp-to-edge), blended
  * between adjacent pyramid levels by the query's mip; slots concatenated

@@ -43,13 +43,15 @@ def lib():
         i32, i64 = ctypes.c_int32, ctypes.c_int64
         L.ntc_oracle_build_bins.argtypes = [P, i64, P, i32, i32, i32, P, P, P, i64, P]
         L.ntc_oracle_divergence.argtypes = [P, i64, P, i32, i32, P, i64, i32, P, P]
+        L.ntc_oracle_divergence_map.argtypes = [P, i32, i32, i32, P, i32, i32, i32, i32, P, P,
+                                                i32, P]
         L.ntc_oracle_features.argtypes = [P, i32, i32, P, P, P, P, P, i64, P, i64, i32, P]
         L.ntc_oracle_decode.argtypes = [P, i32, i32, P, P, P, i32, i32, P, P, P, P, P, i64, P,
                                         i64, i32, P]
         L.ntc_oracle_half_to_double.argtypes = [ctypes.c_uint16]
         L.ntc_oracle_half_to_double.restype = ctypes.c_double
-        for f in ("ntc_oracle_build_bins", "ntc_oracle_divergence", "ntc_oracle_features",
-                  "ntc_oracle_decode"):
+        for f in ("ntc_oracle_build_bins", "ntc_oracle_divergence", "ntc_oracle_divergence_map",
+                  "ntc_oracle_features", "ntc_oracle_decode"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -106,6 +108,24 @@ def divergence(tex_id, tex_to_dec, n_decoders, order=None, wave=64, n_textures=N
     if rc != 0:
         raise OracleError("ntc_oracle_divergence -> %d" % rc)
     return per[: (ln + wave - 1) // wave], tot
+
+
+def divergence_map(tex_id, width, height, tex_to_dec, n_decoders, spp=1, block_w=8, block_h=8,
+                   hist_len=65, n_textures=None):
+    """Distinct decoder ids per screen block -> (map [Hb, Wb], histogram, totals[4])."""
+    tex_id, tex_to_dec = _u32(tex_id), _u32(tex_to_dec)
+    assert tex_id.shape[0] == width * height * spp
+    T = tex_to_dec.shape[0] if n_textures is None else n_textures
+    bx, by = (width + block_w - 1) // block_w, (height + block_h - 1) // block_h
+    dmap = np.zeros((by, bx), np.uint32)
+    hist = np.zeros(hist_len, np.uint32)
+    tot = np.zeros(4, np.uint64)
+    rc = lib().ntc_oracle_divergence_map(_p(tex_id), width, height, spp, _p(tex_to_dec), T,
+                                         n_decoders, block_w, block_h, _p(dmap), _p(hist),
+                                         hist_len, _p(tot))
+    if rc != 0:
+        raise OracleError("ntc_oracle_divergence_map -> %d" % rc)
+    return dmap, hist, tot
 
 
 def _grid_args(w):

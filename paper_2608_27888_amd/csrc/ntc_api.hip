@@ -149,4 +149,19 @@ int ntc_divergence_stats(const uint32_t *tex_id, int64_t n, const uint32_t *tex_
                            per_wave_distinct, totals, (hipStream_t)stream);
 }
 
+int ntc_divergence_map(const uint32_t *tex_id, int32_t width, int32_t height, int32_t spp,
+                       const uint32_t *tex_to_dec, int32_t n_textures, int32_t n_decoders,
+                       int32_t block_w, int32_t block_h, uint32_t *map, uint32_t *histogram,
+                       int32_t hist_len, uint64_t *totals, void *stream) {
+  if (!tex_id || !tex_to_dec || !map || !histogram || !totals) return NTC_ERR_ARG;
+  if (width < 1 || height < 1 || spp < 1 || spp > 64 || block_w < 1 || block_h < 1 ||
+      n_textures < 1 || n_decoders < 1 || n_decoders > NTC_MAX_DECODERS || hist_len < 1 ||
+      hist_len > 4096)
+    return NTC_ERR_ARG;
+  if ((int64_t)width * height * spp > kMaxQueries) return NTC_ERR_ARG;
+  return launch_divergence_map(tex_id, width, height, spp, tex_to_dec, n_textures, n_decoders,
+                               block_w, block_h, map, histogram, hist_len, totals,
+                               (hipStream_t)stream);
+}
+
 }  // extern "C"

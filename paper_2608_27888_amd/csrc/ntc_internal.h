@@ -63,6 +63,10 @@ int launch_divergence(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_
                       int32_t n_textures, int32_t n_decoders, const uint32_t *order,
                       int64_t len, int32_t wave, uint32_t *per_wave, uint64_t *totals,
                       hipStream_t stream);
+int launch_divergence_map(const uint32_t *tex_id, int32_t width, int32_t height, int32_t spp,
+                          const uint32_t *tex_to_dec, int32_t n_textures, int32_t n_decoders,
+                          int32_t block_w, int32_t block_h, uint32_t *map, uint32_t *histogram,
+                          int32_t hist_len, uint64_t *totals, hipStream_t stream);
 
 struct DecodeArgs {
   const uint16_t *latents;

@@ -74,7 +74,9 @@ def lib() -> ctypes.CDLL:
         L.ntc_decode.argtypes = [ctypes.POINTER(Grids), ctypes.POINTER(Decoders), P,
                                  ctypes.POINTER(Queries), P, P, i64, i32, P, P]
         L.ntc_divergence_stats.argtypes = [P, i64, P, i32, i32, P, i64, i32, P, P, P]
-        for f in ("ntc_build_bins", "ntc_get_device_error", "ntc_decode", "ntc_divergence_stats"):
+        L.ntc_divergence_map.argtypes = [P, i32, i32, i32, P, i32, i32, i32, i32, P, P, i32, P, P]
+        for f in ("ntc_build_bins", "ntc_get_device_error", "ntc_decode", "ntc_divergence_stats",
+                  "ntc_divergence_map"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -271,3 +273,21 @@ def divergence_stats(tex_id: torch.Tensor, tex_to_dec: torch.Tensor, n_decoders:
         _ptr(tex_id), n, _ptr(tex_to_dec), T, n_decoders, _ptr(order), ln, wave, _ptr(per),
         _ptr(tot), _stream(stream)))
     return per[: (ln + wave - 1) // wave], tot
+
+
+def divergence_map(tex_id: torch.Tensor, width: int, height: int, tex_to_dec: torch.Tensor,
+                   n_decoders: int, spp: int = 1, block_w: int = 8, block_h: int = 8,
+                   hist_len: int = 65, n_textures: Optional[int] = None, stream=None):
+    """Distinct decoders per screen block -> (map int32 [Hb, Wb], histogram int32
+    [hist_len], totals int64 [4])."""
+    T = int(tex_to_dec.numel()) if n_textures is None else int(n_textures)
+    if int(tex_id.numel()) != width * height * spp:
+        raise ValueError("tex_id must hold width * height * spp queries")
+    bx, by = (width + block_w - 1) // block_w, (height + block_h - 1) // block_h
+    dmap = torch.empty((by, bx), dtype=torch.int32, device=tex_id.device)
+    hist = torch.empty(hist_len, dtype=torch.int32, device=tex_id.device)
+    tot = torch.empty(4, dtype=torch.int64, device=tex_id.device)
+    _check("ntc_divergence_map", lib().ntc_divergence_map(
+        _ptr(tex_id), width, height, spp, _ptr(tex_to_dec), T, n_decoders, block_w, block_h,
+        _ptr(dmap), _ptr(hist), hist_len, _ptr(tot), _stream(stream)))
+    return dmap, hist, tot

@@ -122,3 +122,25 @@ def test_divergence_validation(L):
     assert f(FAKE, 10, FAKE, 4, 2, None, 11, 64, FAKE, FAKE, None) == ntc.NTC_ERR_ARG
     assert f(FAKE, 10, FAKE, 4, 2, None, 10, 64, FAKE, None, None) == ntc.NTC_ERR_ARG
     assert f(FAKE, -1, FAKE, 4, 2, None, 0, 64, FAKE, FAKE, None) == ntc.NTC_ERR_ARG
+
+
+def test_divergence_map_validation(L):
+    f = L.ntc_divergence_map
+    ok = dict(tex=FAKE, W=10, H=10, spp=1, t2d=FAKE, T=4, D=2, bw=8, bh=8, map=FAKE, hist=FAKE,
+              hl=9, tot=FAKE)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(a["tex"], a["W"], a["H"], a["spp"], a["t2d"], a["T"], a["D"], a["bw"], a["bh"],
+                 a["map"], a["hist"], a["hl"], a["tot"], None)
+
+    assert call(tex=None) == ntc.NTC_ERR_ARG
+    assert call(t2d=None) == ntc.NTC_ERR_ARG
+    assert call(W=0) == ntc.NTC_ERR_ARG
+    assert call(spp=65) == ntc.NTC_ERR_ARG
+    assert call(bw=0) == ntc.NTC_ERR_ARG
+    assert call(D=4097) == ntc.NTC_ERR_ARG
+    assert call(hl=0) == ntc.NTC_ERR_ARG
+    assert call(hl=4097) == ntc.NTC_ERR_ARG
+    assert call(W=1 << 16, H=1 << 16, spp=2) == ntc.NTC_ERR_ARG

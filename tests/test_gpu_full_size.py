@@ -65,6 +65,15 @@ def check_frame(dev, oracle, w, n_sample, check_stream=True):
     per_b, tot_b = ntc.divergence_stats(q.tex_id, model.tex_to_dec, w.n_decoders,
                                         order=bins.perm[:P])
     assert int(tot_b[3]) == 1
+    if w.screen is not None:
+        W_, H_, spp = w.screen
+        dmap, hist, tot_m = ntc.divergence_map(q.tex_id, W_, H_, model.tex_to_dec, w.n_decoders,
+                                               spp=spp)
+        dmap_o, hist_o, tot_mo = oracle.divergence_map(w.tex_id, W_, H_, w.tex_to_dec,
+                                                       w.n_decoders, spp=spp)
+        assert np.array_equal(u32(dmap), dmap_o)
+        assert np.array_equal(u32(hist), hist_o)
+        assert np.array_equal(tot_m.cpu().numpy().astype(np.uint64), tot_mo)
     y = out.cpu().numpy()
     assert np.all(np.isfinite(y)) and np.all((y >= 0) & (y <= 1))
     sub = sample(w.n, n_sample)

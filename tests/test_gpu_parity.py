@@ -132,6 +132,40 @@ def test_divergence_bit_exact(dev, oracle, name, wave):
     assert int(tot_b[3]) == 1  # binned order: one decoder per wave
 
 
+@pytest.mark.parametrize("name", ["single", "divergent", "clustered4k", "clustered4k_d512",
+                                  "wide_trilinear"])
+@pytest.mark.parametrize("block", [(8, 8), (16, 16), (5, 3), (64, 1)])
+def test_divergence_map_bit_exact(dev, oracle, name, block):
+    w = small(name)
+    W_, H_, spp = w.screen
+    bw, bh = block
+    say(f"[divergence-map] {name} {W_}x{H_}x{spp} block {bw}x{bh}")
+    model, q = ntc.upload(w, dev)
+    dmap, hist, tot = ntc.divergence_map(q.tex_id, W_, H_, model.tex_to_dec, w.n_decoders,
+                                         spp=spp, block_w=bw, block_h=bh, hist_len=9)
+    dmap_o, hist_o, tot_o = oracle.divergence_map(w.tex_id, W_, H_, w.tex_to_dec, w.n_decoders,
+                                                  spp=spp, block_w=bw, block_h=bh, hist_len=9)
+    assert np.array_equal(u32(dmap), dmap_o)
+    assert np.array_equal(u32(hist), hist_o)
+    assert np.array_equal(tot.cpu().numpy().astype(np.uint64), tot_o)
+
+
+def test_divergence_map_invalid_ids(dev, oracle):
+    rng = np.random.default_rng(4)
+    W_, H_, T, D = 61, 29, 17, 5
+    t2d = rng.integers(0, D + 2, T).astype(np.uint32)
+    tex = rng.integers(0, T + 3, W_ * H_).astype(np.uint32)
+    say("[divergence-map] invalid ids")
+    dmap, hist, tot = ntc.divergence_map(torch.from_numpy(tex.view(np.int32)).to(dev), W_, H_,
+                                         torch.from_numpy(t2d.view(np.int32)).to(dev), D,
+                                         block_w=4, block_h=4, hist_len=3, n_textures=T)
+    dmap_o, hist_o, tot_o = oracle.divergence_map(tex, W_, H_, t2d, D, block_w=4, block_h=4,
+                                                  hist_len=3, n_textures=T)
+    assert np.array_equal(u32(dmap), dmap_o)
+    assert np.array_equal(u32(hist), hist_o)
+    assert np.array_equal(tot.cpu().numpy().astype(np.uint64), tot_o)
+
+
 @pytest.mark.parametrize("name", SMALL)
 def test_decode_matches_oracle(dev, oracle, name):
     w = small(name)
