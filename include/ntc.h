@@ -161,8 +161,8 @@ int ntc_get_device_error(const void *workspace, uint64_t *n_invalid, void *strea
  * in {(2, 8), (2, 16), (3, 16)}, the same channel count on every level and
  * dims[0] = their sum; 3 or 4 layers whose hidden widths are all equal, 64 or
  * 128; dims[n_layers] in {4, 8, 12, 16}; level resolutions in 2 .. 16384;
- * latents of one texture < 2^31 values; output of one call <= 2 GiB
- * (n * dims[n_layers] * 4 bytes).  Other malformed shapes give NTC_ERR_ARG.
+ * latents of one texture < 2^31 values; output of one call at most
+ * 4 GiB - 512 bytes (n * dims[n_layers] * 4 bytes).  Other malformed shapes give NTC_ERR_ARG.
  */
 int ntc_decode(const ntc_grids *grids, const ntc_decoders *decoders,
                const uint32_t *tex_to_dec, const ntc_queries *queries,

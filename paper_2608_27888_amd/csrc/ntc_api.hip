@@ -108,7 +108,7 @@ int ntc_decode(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex_to
   const int out_dim = m->dims[nl];
   if (out_dim > 16 || out_dim % 4 != 0) return NTC_ERR_UNSUPPORTED;
   // one buffer resource with 32-bit byte offsets covers the output
-  if (q->n * (int64_t)out_dim * 4 > 0x7FFFFFF0LL) return NTC_ERR_UNSUPPORTED;
+  if (q->n * (int64_t)out_dim * 4 > kMaxOutBytes) return NTC_ERR_UNSUPPORTED;
   int64_t dec_stride = 0;
   for (int i = 0; i < nl; ++i) dec_stride += (int64_t)m->dims[i + 1] * (m->dims[i] + 1);
 

@@ -467,12 +467,14 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
 
 // Raw buffer resource over the output rows: a store whose byte offset lies past
 // the range is dropped by the hardware, so masked lanes need no branch and
-// every path issues the same number of stores.
-constexpr uint32_t kDropOffset = 0x80000000u;  // past any output range (< 2 GiB)
+// every path issues the same number of stores.  The output is at most
+// kMaxOutBytes, so the drop offset (and the few 16-byte steps added to it) is
+// past the range and offset + 16 never wraps around 32 bits.
+constexpr uint32_t kDropOffset = 0xFFFFFF00u;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_resource(const DecodeArgs &a) {
-  return __builtin_amdgcn_make_buffer_rsrc(a.out, 0, (int)(a.n * (uint32_t)a.out_dim * 4u),
-                                           0x00020000);
+  const uint32_t bytes = a.n * (uint32_t)a.out_dim * 4u;  // <= kMaxOutBytes
+  return __builtin_amdgcn_make_buffer_rsrc(a.out, 0, (int)bytes, 0x00020000);
 }
 
 // Decoded values this lane stores for one 32-query column block: rows 4h..4h+3

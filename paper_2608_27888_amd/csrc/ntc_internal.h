@@ -41,6 +41,9 @@ __device__ __forceinline__ uint32_t xcd_local_block(uint32_t b, uint32_t nblocks
 
 // ------------------------------------------------------------ host helpers
 
+// Largest output of one decode call: byte offsets into it are 32-bit.
+constexpr int64_t kMaxOutBytes = 0xFFFFFE00LL;
+
 struct BinsLayout {
   int64_t chunk;      // queries per workgroup
   int64_t blocks;     // workgroups of the histogram / scatter kernels

@@ -337,6 +337,32 @@ def wide_trilinear(seed: int = 0, width: int = 3840, height: int = 2160, spp: in
                     tex, uv, mip, (width, height, spp), {"voronoi_sites": n_sites})
 
 
+def k_per_wave(seed: int = 0, side: int = 512, k: int = 5, n_textures: int = 10) -> Workload:
+    """The layout of the paper's timing study (Sec. 4.4, Tables performance_5dec and
+    performance_10dec): a side x side output image, one query per pixel in row-major
+    order, and k decoders spread uniformly over every 64-query wave (lane l of a wave
+    uses decoder l mod k; k = 1 is the shared decoder).  Each decoder has its own
+    texture; grids and MLP as the clustered 4K workload (256^2x16 + 128^2x16,
+    32->64->64->8); uv screen-coherent over the image.
+    """
+    if not 1 <= k <= n_textures:
+        raise ValueError("need 1 <= k <= n_textures")
+    res, ch, dims = [256, 128], [16, 16], [32, 64, 64, 8]
+    T = n_textures
+    lat = draw_latents(seed, T, res, ch)
+    par = draw_decoders(seed, T, dims)
+    t2d = np.arange(T, dtype=np.uint32)
+    rng = _rng(seed, _STREAM_QUERIES)
+    xs, ys = _pixels(side, side, 1)
+    u, v = _jittered_uv(rng, side, side, 1, xs, ys)
+    tex = (np.arange(side * side, dtype=np.int64) % kWaveLanes % k).astype(np.uint32)
+    return Workload(f"k{k}_per_wave_{side}", T, res, ch, lat, T, dims, par, t2d, tex,
+                    _to_f32_uv(u, v), None, (side, side, 1), {"k": k})
+
+
+kWaveLanes = 64  # queries per wave of the decode kernels
+
+
 def make(name: str, seed: int = 0, **kw) -> Workload:
     gens = {"tiny": tiny, "single": single, "divergent": divergent,
             "clustered4k": clustered4k, "wide_trilinear": wide_trilinear}
@@ -365,4 +391,6 @@ def small(name: str, seed: int = 0) -> Workload:
         return wide_trilinear(seed, 161, 97, 4, n_decoders=8, n_textures=16)
     if name == "wide_trilinear_d512":
         return wide_trilinear(seed, 161, 97, 4, n_decoders=16, n_textures=16)
+    if name in ("k5_per_wave", "k10_per_wave"):
+        return k_per_wave(seed, 99, int(name[1:name.index("_")]))
     raise KeyError(name)

@@ -106,7 +106,8 @@ def test_decode_validation(L):
     assert _decode(L, dims=(32, 96, 96, 8)) == ntc.NTC_ERR_UNSUPPORTED  # width not built
     assert _decode(L, dims=(32, 64, 64, 20)) == ntc.NTC_ERR_UNSUPPORTED  # too many outputs
     assert _decode(L, dims=(32, 64, 64, 3)) == ntc.NTC_ERR_UNSUPPORTED   # not a multiple of 4
-    assert _decode(L, n=1 << 26) == ntc.NTC_ERR_UNSUPPORTED              # output over 2 GiB
+    assert _decode(L, n=1 << 27, dims=(32, 64, 64, 8)) == ntc.NTC_ERR_UNSUPPORTED  # > 4 GiB
+    assert _decode(L, n=(1 << 27) - 16, dims=(32, 64, 64, 4)) != ntc.NTC_ERR_UNSUPPORTED  # 2 GiB
     assert _decode(L, dims=(32, 8)) == ntc.NTC_ERR_UNSUPPORTED          # no hidden layer
     assert _decode(L, res=(256, 128), ch=(16, 8), dims=(24, 64, 8)) == ntc.NTC_ERR_UNSUPPORTED
     assert _decode(L, res=(0, 128)) == ntc.NTC_ERR_ARG

@@ -128,3 +128,8 @@ def test_full_wide_trilinear_d8(dev, oracle, wide):
 def test_full_wide_trilinear_d512(dev, oracle, wide):
     w = wide.with_decoders(512, np.arange(512, dtype=np.uint32))
     check_frame(dev, oracle, w, 8192, check_stream=False)
+
+
+def test_full_output_past_2gib(dev, oracle):
+    """8192^2 queries x 8 fp32 channels = 2 GiB of output: byte offsets past 2^31."""
+    check_frame(dev, oracle, W.k_per_wave(0, 8192, 5), 8192)

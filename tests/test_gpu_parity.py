@@ -19,7 +19,7 @@ pytestmark = pytest.mark.gpu
 
 TOL = 2e-3
 SMALL = ["tiny", "single", "divergent", "clustered4k", "clustered4k_d512", "wide_trilinear",
-         "wide_trilinear_d512"]
+         "wide_trilinear_d512", "k5_per_wave", "k10_per_wave"]
 
 
 def say(*a):

@@ -1,5 +1,6 @@
 """The seeded input recipes have the structure they claim."""
 import numpy as np
+import pytest
 
 from paper_2608_27888_amd import workloads as W
 
@@ -38,3 +39,13 @@ def test_reproducible():
     assert np.array_equal(a.uv, b.uv) and np.array_equal(a.latents, b.latents)
     c = W.small("clustered4k_d512", seed=3)  # same queries and grids, other decoders
     assert np.array_equal(a.tex_id, c.tex_id) and np.array_equal(a.latents, c.latents)
+
+
+@pytest.mark.parametrize("k", [1, 5, 10])
+def test_k_per_wave_has_k_decoders_in_every_wave(oracle, k):
+    """The timing-study layout of Sec. 4.4: every 64-query wave holds exactly k decoders."""
+    w = W.k_per_wave(0, 96, k)
+    per, tot = oracle.divergence(w.tex_id, w.tex_to_dec, w.n_decoders, wave=64)
+    full = per[: w.n // 64]
+    assert np.all(full == k)
+    assert w.screen == (96, 96, 1) and w.n == 96 * 96
