@@ -273,8 +273,8 @@ def main():
                     ntc.decode(m, q, None, out=out, stream=stream)
             return timed(f, reps, 2, torch) * 1e3
 
-        t = {"d16_binned": ms_step,
-             "d16_stream": run(model, w.n_decoders, bins, False),
+        t = {f"d{w.n_decoders}_binned": ms_step,
+             f"d{w.n_decoders}_stream": run(model, w.n_decoders, bins, False),
              f"d{T}_binned": run(m512, T, bins512, True),
              f"d{T}_stream": run(m512, T, bins512, False)}
         _, ts512 = ntc.divergence_stats(q.tex_id, m512.tex_to_dec, T)

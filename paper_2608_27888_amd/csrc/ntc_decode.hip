@@ -96,14 +96,14 @@ __host__ __device__ inline Image image_of(int n_hidden) {
 
 // Copies decoder `dec` into the LDS image, re-arranged into A fragments; all
 // threads of the workgroup take part; the caller brackets it with barriers.
-template <int NL, int CH, int HID>
+template <int NL, int CH, int HID, int THREADS>
 __device__ void stage_decoder(const DecodeArgs &a, uint32_t dec, uint32_t *lds) {
   using S = Shape<NL, CH, HID>;
   const Image im = image_of<NL, CH, HID>(a.n_hidden);
   const uint16_t *p = a.params + (size_t)dec * (size_t)a.dec_stride;
   const int n_layers = a.n_hidden + 2;
   // fragment lane-slices: one 16-byte lane slice per iteration
-  for (int lf = threadIdx.x; lf < im.n_frags * kWave; lf += kBlock) {
+  for (int lf = threadIdx.x; lf < im.n_frags * kWave; lf += THREADS) {
     const int f = lf / kWave, lane = lf % kWave;
     int layer, mb, s, ks, din, dout;
     if (f < S::MB * S::KS0) {
@@ -145,7 +145,7 @@ __device__ void stage_decoder(const DecodeArgs &a, uint32_t dec, uint32_t *lds) 
   }
   // biases, converted to fp32; rows past the layer width are zero
   float *bias = (float *)(lds + im.bias_off);
-  for (int i = threadIdx.x; i < im.n_bias; i += kBlock) {
+  for (int i = threadIdx.x; i < im.n_bias; i += THREADS) {
     int layer, row, dout;
     if (i < HID * (1 + a.n_hidden)) {
       layer = i / HID; row = i % HID; dout = HID;
@@ -565,6 +565,7 @@ struct Group {
   uint32_t t, n, d, be;
 };
 
+template <int WAVES>
 __device__ __forceinline__ Group group_at(const DecodeArgs &a, uint32_t t, uint32_t d,
                                           uint32_t be, uint32_t D, uint32_t t_end) {
   while (t >= be && d + 1 < D) {  // next non-empty bin
@@ -572,23 +573,33 @@ __device__ __forceinline__ Group group_at(const DecodeArgs &a, uint32_t t, uint3
     be = bin_off(a, d + 1) / kWave;
   }
   const uint32_t n =
-      (t >= be || t >= t_end) ? 0u : min(min((uint32_t)kWavesPerBlock, be - t), t_end - t);
+      (t >= be || t >= t_end) ? 0u : min(min((uint32_t)WAVES, be - t), t_end - t);
   return Group{t, n, d, be};
 }
 
+template <int WAVES>
 __device__ __forceinline__ Group next_group(const DecodeArgs &a, const Group &g, uint32_t D,
                                             uint32_t t_end) {
-  return g.n ? group_at(a, g.t + g.n, g.d, g.be, D, t_end) : g;
+  return g.n ? group_at<WAVES>(a, g.t + g.n, g.d, g.be, D, t_end) : g;
 }
 
-// Workgroups per CU the register allocation must allow: 4 (4 waves per SIMD,
-// <= 128 VGPRs) for 64-wide decoders, 2 for 128-wide ones.
+// Waves per workgroup.  The staged decoder is shared by a workgroup's waves; a
+// 128-wide decoder's LDS image (about 86 KB for 48-128-128-128-8) allows one
+// workgroup per CU, so those workgroups have 8 waves (two per SIMD) rather
+// than 4.
 template <int HID>
-constexpr int kMinBlocks = HID <= 64 ? 4 : 2;
+constexpr int kWaves = HID <= 64 ? 4 : 8;
+template <int HID>
+constexpr int kThreads = kWaves<HID> * kWave;
+// Workgroups per CU the register allocation must allow: 4 for 64-wide decoders
+// (4 waves per SIMD, <= 128 VGPRs), 1 for 128-wide ones (2 waves per SIMD).
+template <int HID>
+constexpr int kMinBlocks = HID <= 64 ? 4 : 1;
 
 template <int NL, int CH, int HID, int NH, bool MIP>
-__global__ void __launch_bounds__(kBlock, kMinBlocks<HID>)
+__global__ void __launch_bounds__(kThreads<HID>, kMinBlocks<HID>)
 decode_binned(const DecodeArgs a) {
+  constexpr int WAVES = kWaves<HID>;
   using S = Shape<NL, CH, HID>;
   extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
   const uint32_t w = threadIdx.x / kWave, lane = lane_id();
@@ -611,10 +622,10 @@ decode_binned(const DecodeArgs a) {
   // Tiles go in groups of up to four consecutive tiles of one bin, tile t + w to
   // wave w; every wave walks the same (uniform) sequence of groups.  A wave
   // without a tile in a group runs it with every lane masked.
-  Group g0 = group_at(a, t, lo, bin_off(a, lo + 1) / kWave, D, t_end);
-  Group g1 = next_group(a, g0, D, t_end);
-  Group g2 = next_group(a, g1, D, t_end);
-  Group g3 = next_group(a, g2, D, t_end);
+  Group g0 = group_at<WAVES>(a, t, lo, bin_off(a, lo + 1) / kWave, D, t_end);
+  Group g1 = next_group<WAVES>(a, g0, D, t_end);
+  Group g2 = next_group<WAVES>(a, g1, D, t_end);
+  Group g3 = next_group<WAVES>(a, g2, D, t_end);
   // perm entry of this wave's tile in group g.  The load is unconditional (slot
   // 0 exists whenever there is a tile) and the entry stays raw until it is
   // used, with `has` saying whether the wave has a tile in the group: selecting
@@ -635,7 +646,7 @@ decode_binned(const DecodeArgs a) {
   // prefetch has a whole tile of work to land.
   auto restage = [&](uint32_t d) {
     __syncthreads();  // every wave is done with the previous decoder
-    stage_decoder<NL, CH, HID>(a, d, lds);
+    stage_decoder<NL, CH, HID, kThreads<HID>>(a, d, lds);
     __syncthreads();
   };
   const Slot s0 = slot_query(g0);
@@ -692,7 +703,7 @@ decode_binned(const DecodeArgs a) {
     g0 = g1;
     g1 = g2;
     g2 = g3;
-    g3 = next_group(a, g3, D, t_end);
+    g3 = next_group<WAVES>(a, g3, D, t_end);
   };
   // Unrolled by two with the prefetch registers swapping roles, so a fetched
   // value is never copied between registers (a copy would wait for the fetch).
@@ -707,22 +718,23 @@ decode_binned(const DecodeArgs a) {
 }
 
 template <int NL, int CH, int HID, int NH, bool MIP>
-__global__ void __launch_bounds__(kBlock, kMinBlocks<HID>)
+__global__ void __launch_bounds__(kThreads<HID>, kMinBlocks<HID>)
 decode_stream(const DecodeArgs a) {
+  constexpr int WAVES = kWaves<HID>;
   using S = Shape<NL, CH, HID>;
   extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
-  __shared__ uint32_t next_dec[2][kWavesPerBlock];
+  __shared__ uint32_t next_dec[2][WAVES];
   const uint32_t w = threadIdx.x / kWave, lane = lane_id();
   const __amdgpu_buffer_rsrc_t out_rsrc = out_resource(a);
   const uint32_t n_tiles = (a.n + kWave - 1) / kWave;
-  const uint32_t n_groups = (n_tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+  const uint32_t n_groups = (n_tiles + WAVES - 1) / WAVES;
   const uint32_t per = (n_groups + gridDim.x - 1) / gridDim.x;
   const uint32_t blk = xcd_local_block(blockIdx.x, gridDim.x);
   const uint32_t g_begin = blk * per, g_end = min(g_begin + per, n_groups);
   uint32_t staged = 0xFFFFFFFFu;
   int parity = 0;
   for (uint32_t g = g_begin; g < g_end; ++g) {
-    const uint32_t q = (g * kWavesPerBlock + w) * kWave + lane;
+    const uint32_t q = (g * WAVES + w) * kWave + lane;
     const Query qq = validate(a, load_query<NL, MIP>(a, q, true));
     uint32_t dq = 0xFFFFFFFFu;
     bool live = qq.valid;
@@ -743,11 +755,11 @@ decode_stream(const DecodeArgs a) {
       __syncthreads();
       uint32_t d = next_dec[parity][0];
 #pragma unroll
-      for (int k = 1; k < kWavesPerBlock; ++k) d = min(d, next_dec[parity][k]);
+      for (int k = 1; k < WAVES; ++k) d = min(d, next_dec[parity][k]);
       parity ^= 1;
       if (d == 0xFFFFFFFFu) break;
       if (d != staged) {
-        stage_decoder<NL, CH, HID>(a, d, lds);
+        stage_decoder<NL, CH, HID, kThreads<HID>>(a, d, lds);
         __syncthreads();
         staged = d;
       }
@@ -781,20 +793,21 @@ int launch_shape(const DecodeArgs &a, hipStream_t stream) {
   }
   // every workgroup resident at once: one round, no tail of late workgroups
   int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, lds) != hipSuccess ||
+  constexpr int waves = kWaves<HID>, threads = kThreads<HID>;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, lds) != hipSuccess ||
       per_cu < 1)
     per_cu = 1;
   const uint64_t cap = (uint64_t)cus * (uint64_t)per_cu;
   const uint64_t tiles = a.bin_offset ? (uint64_t)a.max_tiles : ((uint64_t)a.n + kWave - 1) / kWave;
-  uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+  uint64_t blocks = (tiles + waves - 1) / waves;
   if (blocks > cap) blocks = cap;
   if (blocks == 0) return NTC_OK;
   if (a.bin_offset)
     hipLaunchKernelGGL((decode_binned<NL, CH, HID, NH, MIP>), dim3((unsigned)blocks),
-                       dim3(kBlock), lds, stream, a);
+                       dim3(threads), lds, stream, a);
   else
     hipLaunchKernelGGL((decode_stream<NL, CH, HID, NH, MIP>), dim3((unsigned)blocks),
-                       dim3(kBlock), lds, stream, a);
+                       dim3(threads), lds, stream, a);
   return hip_status(hipGetLastError());
 }
 
