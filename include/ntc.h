@@ -160,7 +160,7 @@ int ntc_get_device_error(const void *workspace, uint64_t *n_invalid, void *strea
  * Supported shapes (else NTC_ERR_UNSUPPORTED): (n_levels, channels per level)
  * in {(2, 8), (2, 16), (3, 16)}, the same channel count on every level and
  * dims[0] = their sum; 3 or 4 layers whose hidden widths are all equal, 64 or
- * 128; dims[n_layers] in {4, 8, 12, 16}; level resolutions in 2 .. 16384;
+ * 128; dims[n_layers] in 1 .. 16; level resolutions in 2 .. 16384;
  * latents of one texture < 2^31 values; output of one call at most
  * 4 GiB - 512 bytes (n * dims[n_layers] * 4 bytes).  Other malformed shapes give NTC_ERR_ARG.
  */
@@ -168,6 +168,34 @@ int ntc_decode(const ntc_grids *grids, const ntc_decoders *decoders,
                const uint32_t *tex_to_dec, const ntc_queries *queries,
                const uint32_t *bin_offset, const uint32_t *perm, int64_t perm_capacity,
                int32_t align, float *out, void *stream);
+
+#define NTC_ACT_RELU 0       /* hidden activation max(x, 0) */
+#define NTC_ACT_LEAKY_RELU 1 /* hidden activation max(x, slope * x) */
+#define NTC_OUT_F32 0        /* output rows of float */
+#define NTC_OUT_F16 1        /* output rows of fp16 (IEEE binary16 bits, rounded to nearest even) */
+
+/*
+ * Decoder variants of ntc_decode_ex.  The Sec. 4 setup trains its decoders with
+ * LeakyReLU hidden activations and three output channels (RGB); fp16 output
+ * rows halve the bytes the decode writes.
+ */
+typedef struct {
+  int32_t hidden_activation; /* NTC_ACT_RELU or NTC_ACT_LEAKY_RELU */
+  float leaky_slope;         /* NTC_ACT_LEAKY_RELU only: 0 < slope < 1 (held as fp16) */
+  int32_t output_format;     /* NTC_OUT_F32 or NTC_OUT_F16 */
+} ntc_decode_options;
+
+/*
+ * ntc_decode with options (NULL = ReLU and float rows, i.e. ntc_decode).  `out`
+ * holds n * dims[n_layers] elements of the chosen format, rows in original
+ * query order; with NTC_OUT_F16 the bytes are n * dims[n_layers] * 2 (same
+ * 4 GiB - 512 limit).  LeakyReLU is applied to the fp16-rounded pre-activation,
+ * in fp16.  Invalid options give NTC_ERR_ARG; everything else as ntc_decode.
+ */
+int ntc_decode_ex(const ntc_grids *grids, const ntc_decoders *decoders,
+                  const uint32_t *tex_to_dec, const ntc_queries *queries,
+                  const uint32_t *bin_offset, const uint32_t *perm, int64_t perm_capacity,
+                  int32_t align, const ntc_decode_options *options, void *out, void *stream);
 
 /*
  * Divergence per wave-sized block (Sec. 2): for window w = entries

@@ -294,10 +294,12 @@ static int dims_valid(int32_t n_layers, const int32_t *dims) {
 
 /*
  * One decoder on one feature vector: for each layer z_j = b_j + sum_k W_jk h_k
- * (ascending k), ReLU between layers, logistic sigmoid on the last layer.
+ * (ascending k); between layers h = z for z > 0 and slope * z otherwise (ReLU for
+ * slope 0, the LeakyReLU of the Sec. 4 setup for slope > 0); logistic sigmoid on
+ * the last layer.
  */
 static void mlp(const uint16_t *p, int32_t n_layers, const int32_t *dims, const double *x,
-                double *y) {
+                double slope, double *y) {
   double h[256], z[256];
   for (int k = 0; k < dims[0]; ++k) h[k] = x[k];
   for (int i = 0; i < n_layers; ++i) {
@@ -311,7 +313,7 @@ static void mlp(const uint16_t *p, int32_t n_layers, const int32_t *dims, const 
     }
     p = b + dout;
     if (i + 1 < n_layers) {
-      for (int j = 0; j < dout; ++j) h[j] = z[j] > 0.0 ? z[j] : 0.0;
+      for (int j = 0; j < dout; ++j) h[j] = z[j] > 0.0 ? z[j] : slope * z[j];
     } else {
       for (int j = 0; j < dout; ++j) y[j] = 1.0 / (1.0 + exp(-z[j]));
     }
@@ -323,9 +325,9 @@ int ntc_oracle_decode(const uint16_t *latents, int32_t n_textures, int32_t n_lev
                       int32_t n_decoders, int32_t n_layers, const int32_t *dims,
                       const uint32_t *tex_to_dec, const uint32_t *tex_id, const float *uv,
                       const float *mip, int64_t n, const int64_t *subset, int64_t n_sel,
-                      int32_t n_threads, double *out) {
+                      int32_t n_threads, double leaky_slope, double *out) {
   if (!grids_valid(n_levels, res, ch, mip != NULL) || !dims_valid(n_layers, dims) || n < 0 ||
-      n_decoders < 1)
+      n_decoders < 1 || !(leaky_slope >= 0.0 && leaky_slope < 1.0))
     return NTC_ORACLE_ERR_ARG;
   int F = 0;
   for (int l = 0; l < n_levels; ++l) F += ch[l];
@@ -350,7 +352,8 @@ int ntc_oracle_decode(const uint16_t *latents, int32_t n_textures, int32_t n_lev
     double x[256], scratch[256];
     query_features(latents + (size_t)t * stride, n_levels, res, ch, off, uv[2 * q],
                    uv[2 * q + 1], mip ? (double)mip[q] : 0.0, x, scratch);
-    mlp(params + (size_t)d * dec_stride, n_layers, dims, x, out + (size_t)i * out_dim);
+    mlp(params + (size_t)d * dec_stride, n_layers, dims, x, leaky_slope,
+        out + (size_t)i * out_dim);
   }
   return bad ? NTC_ORACLE_ERR_ARG : NTC_ORACLE_OK;
 }

@@ -106,8 +106,10 @@ int ntc_oracle_features(const uint16_t *latents, int32_t n_textures, int32_t n_l
 
 /*
  * Full decode: features as above, then the MLP of decoder tex_to_dec[tex_id[q]]:
- *   z = b_i + W_i h (W_i row-major [d_{i+1}][d_i]); hidden layers ReLU; last
- *   layer logistic sigmoid.  params: per decoder contiguous
+ *   z = b_i + W_i h (W_i row-major [d_{i+1}][d_i]); hidden layers
+ *   h = z > 0 ? z : leaky_slope * z (ReLU for slope 0, the Sec. 4 setup's
+ *   LeakyReLU for 0 < slope < 1); last layer logistic sigmoid.
+ *   params: per decoder contiguous
  *   W0, b0, W1, b1, ... (fp16 bits).  out: [n_sel][dims[n_layers]].
  * Invalid queries (bad tex_id or decoder id) leave their row untouched.
  */
@@ -116,7 +118,7 @@ int ntc_oracle_decode(const uint16_t *latents, int32_t n_textures, int32_t n_lev
                       int32_t n_decoders, int32_t n_layers, const int32_t *dims,
                       const uint32_t *tex_to_dec, const uint32_t *tex_id, const float *uv,
                       const float *mip, int64_t n, const int64_t *subset, int64_t n_sel,
-                      int32_t n_threads, double *out);
+                      int32_t n_threads, double leaky_slope, double *out);
 
 /* fp16 bit pattern -> double (exact). */
 double ntc_oracle_half_to_double(uint16_t h);

@@ -47,7 +47,7 @@ def lib():
                                                 i32, P]
         L.ntc_oracle_features.argtypes = [P, i32, i32, P, P, P, P, P, i64, P, i64, i32, P]
         L.ntc_oracle_decode.argtypes = [P, i32, i32, P, P, P, i32, i32, P, P, P, P, P, i64, P,
-                                        i64, i32, P]
+                                        i64, i32, ctypes.c_double, P]
         L.ntc_oracle_half_to_double.argtypes = [ctypes.c_uint16]
         L.ntc_oracle_half_to_double.restype = ctypes.c_double
         for f in ("ntc_oracle_build_bins", "ntc_oracle_divergence", "ntc_oracle_divergence_map",
@@ -149,8 +149,9 @@ def features(w, subset=None, threads=None, fill=np.nan):
     return out
 
 
-def decode(w, subset=None, threads=None, fill=np.nan):
-    """Decoded channels of each query (rows of invalid queries = fill)."""
+def decode(w, subset=None, threads=None, fill=np.nan, leaky_slope=0.0):
+    """Decoded channels of each query (rows of invalid queries = fill); hidden
+    activation ReLU, or LeakyReLU with 0 < leaky_slope < 1."""
     res, ch = _grid_args(w)
     dims = np.ascontiguousarray(w.dims, dtype=np.int32)
     sub = None if subset is None else np.ascontiguousarray(subset, dtype=np.int64)
@@ -159,7 +160,8 @@ def decode(w, subset=None, threads=None, fill=np.nan):
     rc = lib().ntc_oracle_decode(_p(w.latents), w.n_textures, w.n_levels, _p(res), _p(ch),
                                  _p(w.params), w.n_decoders, w.n_layers, _p(dims),
                                  _p(w.tex_to_dec), _p(w.tex_id), _p(w.uv), _p(w.mip), w.n,
-                                 _p(sub), n_sel, threads or default_threads(), _p(out))
+                                 _p(sub), n_sel, threads or default_threads(),
+                                 float(leaky_slope), _p(out))
     if rc != 0:
         raise OracleError("ntc_oracle_decode -> %d" % rc)
     return out

@@ -64,7 +64,23 @@ int ntc_get_device_error(const void *workspace, uint64_t *n_invalid, void *strea
 int ntc_decode(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex_to_dec,
                const ntc_queries *q, const uint32_t *bin_offset, const uint32_t *perm,
                int64_t perm_capacity, int32_t align, float *out, void *stream) {
+  return ntc_decode_ex(g, m, tex_to_dec, q, bin_offset, perm, perm_capacity, align, nullptr,
+                       out, stream);
+}
+
+int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex_to_dec,
+                  const ntc_queries *q, const uint32_t *bin_offset, const uint32_t *perm,
+                  int64_t perm_capacity, int32_t align, const ntc_decode_options *opt,
+                  void *out, void *stream) {
   if (!g || !m || !q) return NTC_ERR_ARG;
+  ntc_decode_options o = {NTC_ACT_RELU, 0.f, NTC_OUT_F32};
+  if (opt) o = *opt;
+  if (o.hidden_activation != NTC_ACT_RELU && o.hidden_activation != NTC_ACT_LEAKY_RELU)
+    return NTC_ERR_ARG;
+  if (o.hidden_activation == NTC_ACT_LEAKY_RELU && !(o.leaky_slope > 0.f && o.leaky_slope < 1.f))
+    return NTC_ERR_ARG;
+  if (o.output_format != NTC_OUT_F32 && o.output_format != NTC_OUT_F16) return NTC_ERR_ARG;
+  const int64_t elem = o.output_format == NTC_OUT_F16 ? 2 : 4;
   if (q->n < 0 || q->n > kMaxQueries) return NTC_ERR_ARG;
   if (g->n_textures < 1 || g->n_levels < 1 || g->n_levels > NTC_MAX_LEVELS) return NTC_ERR_ARG;
   if (m->n_decoders < 1 || m->n_decoders > NTC_MAX_DECODERS || m->n_layers < 1 ||
@@ -106,9 +122,9 @@ int ntc_decode(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex_to
   for (int i = 1; i < nl; ++i)
     if (m->dims[i] != hid) return NTC_ERR_UNSUPPORTED;
   const int out_dim = m->dims[nl];
-  if (out_dim > 16 || out_dim % 4 != 0) return NTC_ERR_UNSUPPORTED;
+  if (out_dim > 16) return NTC_ERR_UNSUPPORTED;
   // one buffer resource with 32-bit byte offsets covers the output
-  if (q->n * (int64_t)out_dim * 4 > kMaxOutBytes) return NTC_ERR_UNSUPPORTED;
+  if (q->n * (int64_t)out_dim * elem > kMaxOutBytes) return NTC_ERR_UNSUPPORTED;
   int64_t dec_stride = 0;
   for (int i = 0; i < nl; ++i) dec_stride += (int64_t)m->dims[i + 1] * (m->dims[i] + 1);
 
@@ -131,6 +147,10 @@ int ntc_decode(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex_to
   a.max_tiles = binned ? (uint32_t)((ntc_bins_capacity(q->n, m->n_decoders, align) + 63) / 64)
                        : (uint32_t)((q->n + 63) / 64);
   a.out = out;
+  a.leaky = o.hidden_activation == NTC_ACT_LEAKY_RELU;
+  const _Float16 slope = (_Float16)o.leaky_slope;
+  a.slope_h2 = (uint32_t)__builtin_bit_cast(uint16_t, slope) * 0x00010001u;
+  a.out_f16 = o.output_format == NTC_OUT_F16;
   if (q->n == 0) return NTC_OK;
   return launch_decode(a, L, ch, F, hid, (hipStream_t)stream);
 }

@@ -41,6 +41,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float float2v __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short short2v __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;
@@ -388,13 +389,31 @@ __device__ __forceinline__ uint32_t relu_pack2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(h, short2v{0, 0}));
 }
 
-// ReLU + fp16 of one 32-row output block -> two K-slices of the next layer.
-__device__ __forceinline__ void relu_pack(const floatx16 &acc, half8 &s0, half8 &s1) {
+// fp16 pair with LeakyReLU max(x, slope * x) (0 < slope < 1) applied on the
+// packed halves, after rounding.
+__device__ __forceinline__ uint32_t leaky_pack2(float a, float b, uint32_t slope_h2) {
+  const half2v h = __builtin_bit_cast(half2v, pack_half2(a, b));
+  const half2v s = __builtin_bit_cast(half2v, slope_h2);
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(h, h * s));
+}
+
+// Hidden activation + fp16 of one 32-row output block -> two K-slices of the
+// next layer.  `leaky` is uniform over the launch.
+__device__ __forceinline__ void relu_pack(const floatx16 &acc, half8 &s0, half8 &s1,
+                                          uint32_t leaky, uint32_t slope_h2) {
   u32x4 a, b;
+  if (!leaky) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    a[i] = relu_pack2(acc[2 * i], acc[2 * i + 1]);
-    b[i] = relu_pack2(acc[8 + 2 * i], acc[8 + 2 * i + 1]);
+    for (int i = 0; i < 4; ++i) {
+      a[i] = relu_pack2(acc[2 * i], acc[2 * i + 1]);
+      b[i] = relu_pack2(acc[8 + 2 * i], acc[8 + 2 * i + 1]);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      a[i] = leaky_pack2(acc[2 * i], acc[2 * i + 1], slope_h2);
+      b[i] = leaky_pack2(acc[8 + 2 * i], acc[8 + 2 * i + 1], slope_h2);
+    }
   }
   s0 = as_half8(a);
   s1 = as_half8(b);
@@ -410,7 +429,7 @@ template <int NL, int CH, int HID, int NH>
 __device__ __forceinline__ void run_mlp(const uint32_t *lds,
                                         const half8 (&xb0)[NL * CH / 16],
                                         const half8 (&xb1)[NL * CH / 16], floatx16 &y0,
-                                        floatx16 &y1) {
+                                        floatx16 &y1, uint32_t leaky, uint32_t slope_h2) {
   using S = Shape<NL, CH, HID>;
   const float *bias = (const float *)(lds) + image_of<NL, CH, HID>(NH).bias_off;
   half8 h0[S::KSH], h1[S::KSH];
@@ -424,8 +443,8 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
       c0 = mfma(w, xb0[s], c0);
       c1 = mfma(w, xb1[s], c1);
     }
-    relu_pack(c0, h0[2 * mb], h0[2 * mb + 1]);
-    relu_pack(c1, h1[2 * mb], h1[2 * mb + 1]);
+    relu_pack(c0, h0[2 * mb], h0[2 * mb + 1], leaky, slope_h2);
+    relu_pack(c1, h1[2 * mb], h1[2 * mb + 1], leaky, slope_h2);
   }
   int frag = S::MB * S::KS0;
   const float *bl = bias + HID;
@@ -442,8 +461,8 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
         c0 = mfma(w, h0[s], c0);
         c1 = mfma(w, h1[s], c1);
       }
-      relu_pack(c0, n0[2 * mb], n0[2 * mb + 1]);
-      relu_pack(c1, n1[2 * mb], n1[2 * mb + 1]);
+      relu_pack(c0, n0[2 * mb], n0[2 * mb + 1], leaky, slope_h2);
+      relu_pack(c1, n1[2 * mb], n1[2 * mb + 1], leaky, slope_h2);
     }
 #pragma unroll
     for (int s = 0; s < S::KSH; ++s) {
@@ -473,14 +492,23 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
 constexpr uint32_t kDropOffset = 0xFFFFFF00u;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_resource(const DecodeArgs &a) {
-  const uint32_t bytes = a.n * (uint32_t)a.out_dim * 4u;  // <= kMaxOutBytes
+  const uint32_t bytes = a.n * (uint32_t)a.out_dim * (a.out_f16 ? 2u : 4u);  // <= kMaxOutBytes
   return __builtin_amdgcn_make_buffer_rsrc(a.out, 0, (int)bytes, 0x00020000);
 }
 
+// How a column block's rows reach memory: fp32 or fp16 runs of 4 rows (output
+// width a multiple of 4), or one store per row (any width, either format).
+enum StoreMode { kStoreF32x4 = 0, kStoreF16x4 = 1, kStoreEach = 2 };
+
+// Store instructions per 32-query column block; fixed for a mode, so the wait
+// counts of the software pipeline do not depend on the data.
+template <int STORE>
+constexpr int kStoresPerBlock = STORE == kStoreEach ? 8 : 2;
+
 // Decoded values this lane stores for one 32-query column block: rows 4h..4h+3
-// (lo) and 8+4h..8+4h+3 (hi) of the query in its column, after the sigmoid.
-// The output width is <= 16 and a multiple of 4; hi is computed only when the
-// width reaches it (otherwise its store is dropped and its value is unused).
+// (lo) and 8+4h..8+4h+3 (hi) of the query in its column, after the sigmoid, as
+// fp32 bits.  The output width is <= 16; hi is computed only when the width
+// reaches it (otherwise its stores are dropped and its value is unused).
 struct OutRows {
   u32x4 lo, hi;
 };
@@ -497,30 +525,61 @@ __device__ __forceinline__ OutRows finish_rows(const floatx16 &z, int out_dim) {
   return r;
 }
 
-// Both 16-byte stores are always issued (rows past the width, and masked
+// Every store of the mode is always issued (rows past the width, and masked
 // lanes, get the drop offset), so the number of stores never depends on the
 // data or the width.
+template <int STORE>
 __device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t out, int out_dim, uint32_t q,
-                                           bool ok, const OutRows &r) {
+                                           bool ok, const OutRows &r, uint32_t out_f16) {
   const int h = lane_id() >> 5;
   const uint32_t row = q * (uint32_t)out_dim;
-  const int r0 = 4 * h, r1 = 8 + 4 * h;
-  const uint32_t off0 = ok && r0 < out_dim ? (row + (uint32_t)r0) * 4u : kDropOffset;
-  const uint32_t off1 = ok && r1 < out_dim ? (row + (uint32_t)r1) * 4u : kDropOffset;
-  __builtin_amdgcn_raw_buffer_store_b128(r.lo, out, off0, 0, 0);
-  __builtin_amdgcn_raw_buffer_store_b128(r.hi, out, off1, 0, 0);
+  if constexpr (STORE == kStoreF32x4) {
+    const int r0 = 4 * h, r1 = 8 + 4 * h;
+    const uint32_t off0 = ok && r0 < out_dim ? (row + (uint32_t)r0) * 4u : kDropOffset;
+    const uint32_t off1 = ok && r1 < out_dim ? (row + (uint32_t)r1) * 4u : kDropOffset;
+    __builtin_amdgcn_raw_buffer_store_b128(r.lo, out, off0, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(r.hi, out, off1, 0, 0);
+  } else if constexpr (STORE == kStoreF16x4) {
+    const int r0 = 4 * h, r1 = 8 + 4 * h;
+    const uint32_t off0 = ok && r0 < out_dim ? (row + (uint32_t)r0) * 2u : kDropOffset;
+    const uint32_t off1 = ok && r1 < out_dim ? (row + (uint32_t)r1) * 2u : kDropOffset;
+    const float4 lo = __builtin_bit_cast(float4, r.lo), hi = __builtin_bit_cast(float4, r.hi);
+    const u32x2 lo16 = {pack_half2(lo.x, lo.y), pack_half2(lo.z, lo.w)};
+    const u32x2 hi16 = {pack_half2(hi.x, hi.y), pack_half2(hi.z, hi.w)};
+    __builtin_amdgcn_raw_buffer_store_b64(lo16, out, off0, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b64(hi16, out, off1, 0, 0);
+  } else {
+    const uint32_t es = out_f16 ? 2u : 4u;
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rr = 8 * g + 4 * h + i;
+        const uint32_t off = ok && rr < out_dim ? (row + (uint32_t)rr) * es : kDropOffset;
+        const uint32_t v = g ? r.hi[i] : r.lo[i];
+        if (out_f16) {
+          const _Float16 f = (_Float16)__builtin_bit_cast(float, v);
+          __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, f), out, off, 0, 0);
+        } else {
+          __builtin_amdgcn_raw_buffer_store_b32(v, out, off, 0, 0);
+        }
+      }
+    }
+  }
 }
 
 // Column block 0 holds the queries of lanes 0..31, block 1 those of lanes
 // 32..63; a lane of half h stores, for each block, the query of lane
 // (block * 32 + lane % 32): its own in block h, its partner's in the other.
+template <int STORE>
 __device__ __forceinline__ void store_tile(__amdgpu_buffer_rsrc_t out, int out_dim, uint32_t q,
-                                           bool ok, const OutRows &b0, const OutRows &b1) {
+                                           bool ok, const OutRows &b0, const OutRows &b1,
+                                           uint32_t out_f16) {
   const uint32_t q_other = (uint32_t)__shfl_xor((int)q, 32, kWave);
   const bool ok_other = __shfl_xor((int)ok, 32, kWave) != 0;
   const bool h = lane_id() >= 32;
-  store_rows(out, out_dim, h ? q_other : q, h ? ok_other : ok, b0);
-  store_rows(out, out_dim, h ? q : q_other, h ? ok : ok_other, b1);
+  store_rows<STORE>(out, out_dim, h ? q_other : q, h ? ok_other : ok, b0, out_f16);
+  store_rows<STORE>(out, out_dim, h ? q : q_other, h ? ok : ok_other, b1, out_f16);
 }
 
 // Query data of a slot.  The loads are unconditional (a slot without a valid
@@ -596,7 +655,7 @@ constexpr int kThreads = kWaves<HID> * kWave;
 template <int HID>
 constexpr int kMinBlocks = HID <= 64 ? 4 : 1;
 
-template <int NL, int CH, int HID, int NH, bool MIP>
+template <int NL, int CH, int HID, int NH, bool MIP, int STORE>
 __global__ void __launch_bounds__(kThreads<HID>, kMinBlocks<HID>)
 decode_binned(const DecodeArgs a) {
   constexpr int WAVES = kWaves<HID>;
@@ -665,9 +724,8 @@ decode_binned(const DecodeArgs a) {
   // order, as at its back edge, so the waits at its top need not drain.
   // Distinct offsets keep them from being merged.
 #pragma unroll
-  for (uint32_t i = 0; i < 4; ++i)
-    __builtin_amdgcn_raw_buffer_store_b128(u32x4{0u, 0u, 0u, 0u}, out_rsrc,
-                                           kDropOffset + 16u * i, 0, 0);
+  for (uint32_t i = 0; i < 2 * kStoresPerBlock<STORE>; ++i)
+    __builtin_amdgcn_raw_buffer_store_b32(0u, out_rsrc, kDropOffset + 16u * i, 0, 0);
   // One tile: decode `cur` (taps already in flight), stage the next group's
   // decoder if it changes, fetch the next tile's taps from q_in (its query data),
   // prefetch query data of the tile after from p_in into q_out and the
@@ -681,7 +739,7 @@ decode_binned(const DecodeArgs a) {
     half8 xb0[S::KS0], xb1[S::KS0];
     to_b_operands<S::KS0>(x, xb0, xb1);
     floatx16 z0, z1;
-    run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, z0, z1);
+    run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, z0, z1, a.leaky, a.slope_h2);
     const OutRows r0 = finish_rows(z0, a.out_dim);
     const OutRows r1 = finish_rows(z1, a.out_dim);
     __builtin_amdgcn_sched_barrier(0);
@@ -698,7 +756,7 @@ decode_binned(const DecodeArgs a) {
     q_out = load_query<NL, MIP>(a, p_in.raw, p_in.has);
     p_out = slot_query(g3);
     __builtin_amdgcn_sched_barrier(0);
-    store_tile(out_rsrc, a.out_dim, cur.q, cur.valid, r0, r1);
+    store_tile<STORE>(out_rsrc, a.out_dim, cur.q, cur.valid, r0, r1, a.out_f16);
     cur = nxt;
     g0 = g1;
     g1 = g2;
@@ -717,7 +775,7 @@ decode_binned(const DecodeArgs a) {
   }
 }
 
-template <int NL, int CH, int HID, int NH, bool MIP>
+template <int NL, int CH, int HID, int NH, bool MIP, int STORE>
 __global__ void __launch_bounds__(kThreads<HID>, kMinBlocks<HID>)
 decode_stream(const DecodeArgs a) {
   constexpr int WAVES = kWaves<HID>;
@@ -767,9 +825,9 @@ decode_stream(const DecodeArgs a) {
       const uint64_t sel = ballot(mine_now);
       if (sel) {
         floatx16 z0, z1;
-        run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, z0, z1);
-        store_tile(out_rsrc, a.out_dim, q, mine_now, finish_rows(z0, a.out_dim),
-                   finish_rows(z1, a.out_dim));
+        run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, z0, z1, a.leaky, a.slope_h2);
+        store_tile<STORE>(out_rsrc, a.out_dim, q, mine_now, finish_rows(z0, a.out_dim),
+                          finish_rows(z1, a.out_dim), a.out_f16);
         todo &= ~sel;
         live = live && !mine_now;
       }
@@ -777,15 +835,15 @@ decode_stream(const DecodeArgs a) {
   }
 }
 
-template <int NL, int CH, int HID, int NH, bool MIP>
+template <int NL, int CH, int HID, int NH, bool MIP, int STORE>
 int launch_shape(const DecodeArgs &a, hipStream_t stream) {
   const Image im = image_of<NL, CH, HID>(NH);
   const size_t lds = (size_t)im.bytes;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess)
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  const void *fn = a.bin_offset ? (const void *)decode_binned<NL, CH, HID, NH, MIP>
-                                : (const void *)decode_stream<NL, CH, HID, NH, MIP>;
+  const void *fn = a.bin_offset ? (const void *)decode_binned<NL, CH, HID, NH, MIP, STORE>
+                                : (const void *)decode_stream<NL, CH, HID, NH, MIP, STORE>;
   if (lds > 64 * 1024) {
     if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
         hipSuccess)
@@ -803,18 +861,25 @@ int launch_shape(const DecodeArgs &a, hipStream_t stream) {
   if (blocks > cap) blocks = cap;
   if (blocks == 0) return NTC_OK;
   if (a.bin_offset)
-    hipLaunchKernelGGL((decode_binned<NL, CH, HID, NH, MIP>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((decode_binned<NL, CH, HID, NH, MIP, STORE>), dim3((unsigned)blocks),
                        dim3(threads), lds, stream, a);
   else
-    hipLaunchKernelGGL((decode_stream<NL, CH, HID, NH, MIP>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((decode_stream<NL, CH, HID, NH, MIP, STORE>), dim3((unsigned)blocks),
                        dim3(threads), lds, stream, a);
   return hip_status(hipGetLastError());
 }
 
+template <int NL, int CH, int HID, int NH, bool MIP>
+int launch_store(const DecodeArgs &a, hipStream_t stream) {
+  if (a.out_dim % 4 != 0) return launch_shape<NL, CH, HID, NH, MIP, kStoreEach>(a, stream);
+  return a.out_f16 ? launch_shape<NL, CH, HID, NH, MIP, kStoreF16x4>(a, stream)
+                   : launch_shape<NL, CH, HID, NH, MIP, kStoreF32x4>(a, stream);
+}
+
 template <int NL, int CH, int HID, int NH>
 int launch_mip(const DecodeArgs &a, hipStream_t stream) {
-  return a.mip ? launch_shape<NL, CH, HID, NH, true>(a, stream)
-               : launch_shape<NL, CH, HID, NH, false>(a, stream);
+  return a.mip ? launch_store<NL, CH, HID, NH, true>(a, stream)
+               : launch_store<NL, CH, HID, NH, false>(a, stream);
 }
 
 template <int NL, int CH, int HID>

@@ -92,7 +92,10 @@ struct DecodeArgs {
   const uint32_t *perm;
   uint64_t perm_capacity;             // entries of perm (binned mode)
   uint32_t max_tiles;                 // upper bound of the tile count (grid sizing)
-  float *out;
+  void *out;
+  uint32_t leaky;                     // hidden activation: 0 ReLU, 1 LeakyReLU
+  uint32_t slope_h2;                  // LeakyReLU slope as an fp16 pair
+  uint32_t out_f16;                   // output rows: 0 fp32, 1 fp16
 };
 
 // Returns NTC_ERR_UNSUPPORTED when no kernel is built for the shape.

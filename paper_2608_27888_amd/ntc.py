@@ -73,10 +73,12 @@ def lib() -> ctypes.CDLL:
         L.ntc_get_device_error.argtypes = [P, P, P]
         L.ntc_decode.argtypes = [ctypes.POINTER(Grids), ctypes.POINTER(Decoders), P,
                                  ctypes.POINTER(Queries), P, P, i64, i32, P, P]
+        L.ntc_decode_ex.argtypes = [ctypes.POINTER(Grids), ctypes.POINTER(Decoders), P,
+                                    ctypes.POINTER(Queries), P, P, i64, i32, P, P, P]
         L.ntc_divergence_stats.argtypes = [P, i64, P, i32, i32, P, i64, i32, P, P, P]
         L.ntc_divergence_map.argtypes = [P, i32, i32, i32, P, i32, i32, i32, i32, P, P, i32, P, P]
-        for f in ("ntc_build_bins", "ntc_get_device_error", "ntc_decode", "ntc_divergence_stats",
-                  "ntc_divergence_map"):
+        for f in ("ntc_build_bins", "ntc_get_device_error", "ntc_decode", "ntc_decode_ex",
+                  "ntc_divergence_stats", "ntc_divergence_map"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -239,21 +241,42 @@ def upload(w, device="cuda"):
     return model, queries
 
 
+NTC_ACT_RELU, NTC_ACT_LEAKY_RELU = 0, 1
+NTC_OUT_F32, NTC_OUT_F16 = 0, 1
+
+
+class DecodeOptions(ctypes.Structure):
+    _fields_ = [("hidden_activation", ctypes.c_int32), ("leaky_slope", ctypes.c_float),
+                ("output_format", ctypes.c_int32)]
+
+
 def decode(model: DeviceModel, queries: DeviceQueries, bins: Optional[Bins] = None,
-           out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """Binned mode when `bins` is given, stream (divergent) mode otherwise."""
+           out: Optional[torch.Tensor] = None, stream=None, leaky_slope: Optional[float] = None,
+           out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
+    """Binned mode when `bins` is given, stream (divergent) mode otherwise.  Hidden
+    activation ReLU, or LeakyReLU max(x, slope x) when leaky_slope is given; output
+    rows float32 or float16."""
+    if out_dtype not in (torch.float32, torch.float16):
+        raise ValueError("out_dtype must be float32 or float16")
     if out is None:
-        out = torch.empty((queries.n, model.out_dim), dtype=torch.float32,
+        out = torch.empty((queries.n, model.out_dim), dtype=out_dtype,
                           device=queries.tex_id.device)
+    elif out.dtype != out_dtype:
+        raise ValueError("out has the wrong dtype")
     g, d, q = model.grids(), model.decoders(), queries.struct()
+    opt = DecodeOptions(NTC_ACT_RELU if leaky_slope is None else NTC_ACT_LEAKY_RELU,
+                        0.0 if leaky_slope is None else float(leaky_slope),
+                        NTC_OUT_F16 if out_dtype == torch.float16 else NTC_OUT_F32)
     if bins is not None:
-        st = lib().ntc_decode(ctypes.byref(g), ctypes.byref(d), _ptr(model.tex_to_dec),
-                              ctypes.byref(q), _ptr(bins.bin_offset), _ptr(bins.perm),
-                              bins.capacity, bins.align, _ptr(out), _stream(stream))
+        st = lib().ntc_decode_ex(ctypes.byref(g), ctypes.byref(d), _ptr(model.tex_to_dec),
+                                 ctypes.byref(q), _ptr(bins.bin_offset), _ptr(bins.perm),
+                                 bins.capacity, bins.align, ctypes.byref(opt), _ptr(out),
+                                 _stream(stream))
     else:
-        st = lib().ntc_decode(ctypes.byref(g), ctypes.byref(d), _ptr(model.tex_to_dec),
-                              ctypes.byref(q), None, None, 0, 0, _ptr(out), _stream(stream))
-    _check("ntc_decode", st)
+        st = lib().ntc_decode_ex(ctypes.byref(g), ctypes.byref(d), _ptr(model.tex_to_dec),
+                                 ctypes.byref(q), None, None, 0, 0, ctypes.byref(opt), _ptr(out),
+                                 _stream(stream))
+    _check("ntc_decode_ex", st)
     return out
 
 

@@ -88,6 +88,16 @@ class Workload:
         """Multiply-adds x 2 of the MLP, unpadded."""
         return int(sum(2 * a * b for a, b in zip(self.dims[:-1], self.dims[1:])))
 
+    def with_dims(self, dims, seed: int = 0) -> "Workload":
+        """Same grids, map and queries; decoders redrawn with layer widths `dims`
+        (dims[0] must stay the feature count)."""
+        assert dims[0] == self.dims[0]
+        params = draw_decoders(seed, self.n_decoders, dims)
+        return Workload(f"{self.name}_mlp{'-'.join(map(str, dims))}", self.n_textures,
+                        list(self.res), list(self.channels), self.latents, self.n_decoders,
+                        list(dims), params, self.tex_to_dec, self.tex_id, self.uv, self.mip,
+                        self.screen, dict(self.meta))
+
     def with_decoders(self, n_decoders: int, tex_to_dec: np.ndarray, seed: int = 0,
                       name: Optional[str] = None) -> "Workload":
         """Same grids and queries, a different decoder set and map."""

@@ -105,7 +105,7 @@ def test_decode_validation(L):
     assert _decode(L, dims=(32, 64, 48, 8)) == ntc.NTC_ERR_UNSUPPORTED  # unequal hidden widths
     assert _decode(L, dims=(32, 96, 96, 8)) == ntc.NTC_ERR_UNSUPPORTED  # width not built
     assert _decode(L, dims=(32, 64, 64, 20)) == ntc.NTC_ERR_UNSUPPORTED  # too many outputs
-    assert _decode(L, dims=(32, 64, 64, 3)) == ntc.NTC_ERR_UNSUPPORTED   # not a multiple of 4
+    assert _decode(L, dims=(32, 64, 64, 3)) != ntc.NTC_ERR_UNSUPPORTED   # RGB rows are built
     assert _decode(L, n=1 << 27, dims=(32, 64, 64, 8)) == ntc.NTC_ERR_UNSUPPORTED  # > 4 GiB
     assert _decode(L, n=(1 << 27) - 16, dims=(32, 64, 64, 4)) != ntc.NTC_ERR_UNSUPPORTED  # 2 GiB
     assert _decode(L, dims=(32, 8)) == ntc.NTC_ERR_UNSUPPORTED          # no hidden layer
@@ -145,3 +145,29 @@ def test_divergence_map_validation(L):
     assert call(hl=0) == ntc.NTC_ERR_ARG
     assert call(hl=4097) == ntc.NTC_ERR_ARG
     assert call(W=1 << 16, H=1 << 16, spp=2) == ntc.NTC_ERR_ARG
+
+
+def test_decode_options_validation(L):
+    g = ntc.Grids()
+    g.n_textures, g.n_levels = 4, 2
+    for i, (r, c) in enumerate(zip((256, 128), (16, 16))):
+        g.res[i], g.channels[i] = r, c
+    g.latents = FAKE
+    d = ntc.Decoders()
+    d.n_decoders, d.n_layers = 4, 3
+    for i, v in enumerate((32, 64, 64, 8)):
+        d.dims[i] = v
+    d.params = FAKE
+    q = ntc.Queries()
+    q.tex_id, q.uv, q.mip, q.n = FAKE, FAKE, None, 100
+
+    def call(act, slope, fmt):
+        o = ntc.DecodeOptions(act, slope, fmt)
+        return L.ntc_decode_ex(ctypes.byref(g), ctypes.byref(d), FAKE, ctypes.byref(q), None,
+                               None, 0, 0, ctypes.byref(o), FAKE, None)
+
+    assert call(2, 0.0, 0) == ntc.NTC_ERR_ARG                 # unknown activation
+    assert call(ntc.NTC_ACT_LEAKY_RELU, 0.0, 0) == ntc.NTC_ERR_ARG
+    assert call(ntc.NTC_ACT_LEAKY_RELU, 1.0, 0) == ntc.NTC_ERR_ARG
+    assert call(ntc.NTC_ACT_RELU, 0.0, 2) == ntc.NTC_ERR_ARG  # unknown output format
+    assert call(ntc.NTC_ACT_LEAKY_RELU, 0.01, ntc.NTC_OUT_F16) != ntc.NTC_ERR_ARG

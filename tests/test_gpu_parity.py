@@ -183,6 +183,58 @@ def test_decode_matches_oracle(dev, oracle, name):
     assert np.all((yb >= 0) & (yb <= 1))
 
 
+VARIANTS = [  # (config, MLP widths or None, LeakyReLU slope or None, output dtype)
+    ("clustered4k", None, 0.01, torch.float32),
+    ("clustered4k", None, None, torch.float16),
+    ("clustered4k", [32, 64, 64, 3], 0.01, torch.float32),
+    ("clustered4k", [32, 64, 64, 3], 0.01, torch.float16),
+    ("clustered4k", [32, 64, 64, 5], None, torch.float32),
+    ("single", [32, 64, 64, 64, 12], 0.05, torch.float16),
+    ("tiny", [16, 64, 64, 3], 0.01, torch.float16),
+    ("wide_trilinear", [48, 128, 128, 128, 3], 0.01, torch.float16),
+]
+
+
+@pytest.mark.parametrize("name,dims,slope,dtype", VARIANTS)
+def test_decode_variants(dev, oracle, name, dims, slope, dtype):
+    """LeakyReLU hidden layers, RGB and other widths, fp16 output rows (Sec. 4 setup)."""
+    w = small(name)
+    if dims is not None:
+        w = w.with_dims(dims, seed=3)
+    say(f"[variant] {name} dims={w.dims} slope={slope} {dtype}")
+    model, q = ntc.upload(w, dev)
+    bins = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders)
+    out_b = ntc.decode(model, q, bins, leaky_slope=slope, out_dtype=dtype)
+    out_s = ntc.decode(model, q, leaky_slope=slope, out_dtype=dtype)
+    ref = oracle.decode(w, leaky_slope=slope or 0.0)
+    yb = out_b.cpu().numpy()
+    err = np.abs(yb.astype(np.float64) - ref).max()
+    say(f"    max abs err {err:.3e}")
+    assert err <= TOL
+    assert torch.equal(out_b.view(torch.int16 if dtype == torch.float16 else torch.int32),
+                       out_s.view(torch.int16 if dtype == torch.float16 else torch.int32))
+    if dtype == torch.float16:
+        # fp16 rows are the fp32 rows rounded to nearest even
+        f32 = ntc.decode(model, q, bins, leaky_slope=slope, out_dtype=torch.float32)
+        assert torch.equal(f32.half().view(torch.int16), out_b.view(torch.int16))
+
+
+def test_decode_fp16_rows_untouched_for_invalid_queries(dev, oracle):
+    w = W.small("tiny").with_dims([16, 64, 64, 3], seed=1)
+    w.tex_id = w.tex_id.copy()
+    w.tex_id[::11] = 9
+    say("[variant] invalid queries, fp16 rows")
+    model, q = ntc.upload(w, dev)
+    bins = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders)
+    out = torch.full((w.n, 3), -7.0, dtype=torch.float16, device=dev)
+    ntc.decode(model, q, bins, out=out, leaky_slope=0.01, out_dtype=torch.float16)
+    ref = oracle.decode(w, leaky_slope=0.01)
+    bad = np.isnan(ref[:, 0])
+    o = out.cpu().numpy()
+    assert bad.sum() > 0 and np.all(o[bad] == -7.0)
+    assert np.abs(o[~bad].astype(np.float64) - ref[~bad]).max() <= TOL
+
+
 def test_decode_is_deterministic(dev):
     w = small("clustered4k")
     say("[determinism] clustered4k")

@@ -206,3 +206,24 @@ def test_subset_matches_full(oracle):
     full = oracle.decode(w)
     sub = np.array([499, 0, 17, 17, 250])
     assert np.array_equal(oracle.decode(w, subset=sub), full[sub])
+
+
+@pytest.mark.parametrize("slope", [0.01, 0.2])
+def test_leaky_identity_chain_gives_sigmoid_of_leaky_features(oracle, slope):
+    """Two identity layers around one LeakyReLU (the Sec. 4 setup's activation):
+    y = sigmoid(x) where x > 0 and sigmoid(slope * x) elsewhere."""
+    dims = [8, 8, 8]
+    eye = np.concatenate([np.eye(8).ravel(), np.zeros(8)])
+    w = make_workload([16], [8], T=2, dims=dims, D=1, n=400, seed=19,
+                      params=W.fp16_bits(np.concatenate([eye, eye])))
+    x = oracle.features(w)
+    h = np.where(x > 0, x, slope * x)
+    np.testing.assert_allclose(oracle.decode(w, leaky_slope=slope), 1.0 / (1.0 + np.exp(-h)),
+                               rtol=4e-16, atol=0)
+    assert np.any(x < 0)
+
+
+def test_leaky_slope_zero_is_relu(oracle):
+    w = make_workload([16, 8], [8, 8], T=4, dims=[16, 32, 32, 3], D=2, n=300, seed=21)
+    assert np.array_equal(oracle.decode(w, leaky_slope=0.0), oracle.decode(w))
+    assert not np.array_equal(oracle.decode(w, leaky_slope=0.1), oracle.decode(w))
