@@ -398,21 +398,20 @@ __device__ __forceinline__ uint32_t leaky_pack2(float a, float b, uint32_t slope
 }
 
 // Hidden activation + fp16 of one 32-row output block -> two K-slices of the
-// next layer.  `leaky` is uniform over the launch.
+// next layer.  LEAKY selects LeakyReLU; it is a template parameter so that the
+// layer's MFMAs and conversions stay in one basic block.
+template <bool LEAKY>
 __device__ __forceinline__ void relu_pack(const floatx16 &acc, half8 &s0, half8 &s1,
-                                          uint32_t leaky, uint32_t slope_h2) {
+                                          uint32_t slope_h2) {
   u32x4 a, b;
-  if (!leaky) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      a[i] = relu_pack2(acc[2 * i], acc[2 * i + 1]);
-      b[i] = relu_pack2(acc[8 + 2 * i], acc[8 + 2 * i + 1]);
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < 4; ++i) {
+    if constexpr (LEAKY) {
       a[i] = leaky_pack2(acc[2 * i], acc[2 * i + 1], slope_h2);
       b[i] = leaky_pack2(acc[8 + 2 * i], acc[8 + 2 * i + 1], slope_h2);
+    } else {
+      a[i] = relu_pack2(acc[2 * i], acc[2 * i + 1]);
+      b[i] = relu_pack2(acc[8 + 2 * i], acc[8 + 2 * i + 1]);
     }
   }
   s0 = as_half8(a);
@@ -425,11 +424,11 @@ __device__ __forceinline__ float sigmoid(float z) {
 
 // Runs the staged decoder on the tile's features; returns the output layer's
 // accumulators (sigmoid applied) for the two column blocks.
-template <int NL, int CH, int HID, int NH>
+template <int NL, int CH, int HID, int NH, bool LEAKY>
 __device__ __forceinline__ void run_mlp(const uint32_t *lds,
                                         const half8 (&xb0)[NL * CH / 16],
                                         const half8 (&xb1)[NL * CH / 16], floatx16 &y0,
-                                        floatx16 &y1, uint32_t leaky, uint32_t slope_h2) {
+                                        floatx16 &y1, uint32_t slope_h2) {
   using S = Shape<NL, CH, HID>;
   const float *bias = (const float *)(lds) + image_of<NL, CH, HID>(NH).bias_off;
   half8 h0[S::KSH], h1[S::KSH];
@@ -443,8 +442,8 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
       c0 = mfma(w, xb0[s], c0);
       c1 = mfma(w, xb1[s], c1);
     }
-    relu_pack(c0, h0[2 * mb], h0[2 * mb + 1], leaky, slope_h2);
-    relu_pack(c1, h1[2 * mb], h1[2 * mb + 1], leaky, slope_h2);
+    relu_pack<LEAKY>(c0, h0[2 * mb], h0[2 * mb + 1], slope_h2);
+    relu_pack<LEAKY>(c1, h1[2 * mb], h1[2 * mb + 1], slope_h2);
   }
   int frag = S::MB * S::KS0;
   const float *bl = bias + HID;
@@ -461,8 +460,8 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
         c0 = mfma(w, h0[s], c0);
         c1 = mfma(w, h1[s], c1);
       }
-      relu_pack(c0, n0[2 * mb], n0[2 * mb + 1], leaky, slope_h2);
-      relu_pack(c1, n1[2 * mb], n1[2 * mb + 1], leaky, slope_h2);
+      relu_pack<LEAKY>(c0, n0[2 * mb], n0[2 * mb + 1], slope_h2);
+      relu_pack<LEAKY>(c1, n1[2 * mb], n1[2 * mb + 1], slope_h2);
     }
 #pragma unroll
     for (int s = 0; s < S::KSH; ++s) {
@@ -655,7 +654,7 @@ constexpr int kThreads = kWaves<HID> * kWave;
 template <int HID>
 constexpr int kMinBlocks = HID <= 64 ? 4 : 1;
 
-template <int NL, int CH, int HID, int NH, bool MIP, int STORE>
+template <int NL, int CH, int HID, int NH, bool MIP, int STORE, bool LEAKY>
 __global__ void __launch_bounds__(kThreads<HID>, kMinBlocks<HID>)
 decode_binned(const DecodeArgs a) {
   constexpr int WAVES = kWaves<HID>;
@@ -739,7 +738,7 @@ decode_binned(const DecodeArgs a) {
     half8 xb0[S::KS0], xb1[S::KS0];
     to_b_operands<S::KS0>(x, xb0, xb1);
     floatx16 z0, z1;
-    run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, z0, z1, a.leaky, a.slope_h2);
+    run_mlp<NL, CH, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
     const OutRows r0 = finish_rows(z0, a.out_dim);
     const OutRows r1 = finish_rows(z1, a.out_dim);
     __builtin_amdgcn_sched_barrier(0);
@@ -775,7 +774,7 @@ decode_binned(const DecodeArgs a) {
   }
 }
 
-template <int NL, int CH, int HID, int NH, bool MIP, int STORE>
+template <int NL, int CH, int HID, int NH, bool MIP, int STORE, bool LEAKY>
 __global__ void __launch_bounds__(kThreads<HID>, kMinBlocks<HID>)
 decode_stream(const DecodeArgs a) {
   constexpr int WAVES = kWaves<HID>;
@@ -825,7 +824,7 @@ decode_stream(const DecodeArgs a) {
       const uint64_t sel = ballot(mine_now);
       if (sel) {
         floatx16 z0, z1;
-        run_mlp<NL, CH, HID, NH>(lds, xb0, xb1, z0, z1, a.leaky, a.slope_h2);
+        run_mlp<NL, CH, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
         store_tile<STORE>(out_rsrc, a.out_dim, q, mine_now, finish_rows(z0, a.out_dim),
                           finish_rows(z1, a.out_dim), a.out_f16);
         todo &= ~sel;
@@ -835,15 +834,15 @@ decode_stream(const DecodeArgs a) {
   }
 }
 
-template <int NL, int CH, int HID, int NH, bool MIP, int STORE>
+template <int NL, int CH, int HID, int NH, bool MIP, int STORE, bool LEAKY>
 int launch_shape(const DecodeArgs &a, hipStream_t stream) {
   const Image im = image_of<NL, CH, HID>(NH);
   const size_t lds = (size_t)im.bytes;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess)
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  const void *fn = a.bin_offset ? (const void *)decode_binned<NL, CH, HID, NH, MIP, STORE>
-                                : (const void *)decode_stream<NL, CH, HID, NH, MIP, STORE>;
+  const void *fn = a.bin_offset ? (const void *)decode_binned<NL, CH, HID, NH, MIP, STORE, LEAKY>
+                                : (const void *)decode_stream<NL, CH, HID, NH, MIP, STORE, LEAKY>;
   if (lds > 64 * 1024) {
     if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
         hipSuccess)
@@ -861,25 +860,31 @@ int launch_shape(const DecodeArgs &a, hipStream_t stream) {
   if (blocks > cap) blocks = cap;
   if (blocks == 0) return NTC_OK;
   if (a.bin_offset)
-    hipLaunchKernelGGL((decode_binned<NL, CH, HID, NH, MIP, STORE>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((decode_binned<NL, CH, HID, NH, MIP, STORE, LEAKY>), dim3((unsigned)blocks),
                        dim3(threads), lds, stream, a);
   else
-    hipLaunchKernelGGL((decode_stream<NL, CH, HID, NH, MIP, STORE>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((decode_stream<NL, CH, HID, NH, MIP, STORE, LEAKY>), dim3((unsigned)blocks),
                        dim3(threads), lds, stream, a);
   return hip_status(hipGetLastError());
 }
 
-template <int NL, int CH, int HID, int NH, bool MIP>
+template <int NL, int CH, int HID, int NH, bool MIP, bool LEAKY>
 int launch_store(const DecodeArgs &a, hipStream_t stream) {
-  if (a.out_dim % 4 != 0) return launch_shape<NL, CH, HID, NH, MIP, kStoreEach>(a, stream);
-  return a.out_f16 ? launch_shape<NL, CH, HID, NH, MIP, kStoreF16x4>(a, stream)
-                   : launch_shape<NL, CH, HID, NH, MIP, kStoreF32x4>(a, stream);
+  if (a.out_dim % 4 != 0) return launch_shape<NL, CH, HID, NH, MIP, kStoreEach, LEAKY>(a, stream);
+  return a.out_f16 ? launch_shape<NL, CH, HID, NH, MIP, kStoreF16x4, LEAKY>(a, stream)
+                   : launch_shape<NL, CH, HID, NH, MIP, kStoreF32x4, LEAKY>(a, stream);
+}
+
+template <int NL, int CH, int HID, int NH, bool MIP>
+int launch_act(const DecodeArgs &a, hipStream_t stream) {
+  return a.leaky ? launch_store<NL, CH, HID, NH, MIP, true>(a, stream)
+                 : launch_store<NL, CH, HID, NH, MIP, false>(a, stream);
 }
 
 template <int NL, int CH, int HID, int NH>
 int launch_mip(const DecodeArgs &a, hipStream_t stream) {
-  return a.mip ? launch_store<NL, CH, HID, NH, true>(a, stream)
-               : launch_store<NL, CH, HID, NH, false>(a, stream);
+  return a.mip ? launch_act<NL, CH, HID, NH, true>(a, stream)
+               : launch_act<NL, CH, HID, NH, false>(a, stream);
 }
 
 template <int NL, int CH, int HID>
