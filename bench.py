@@ -36,8 +36,10 @@ def log(*a):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=3)
+    # about 25 ms of work each: the GPU's clocks take several milliseconds of
+    # sustained load to settle, and short warm-ups time the ramp instead
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=100)
     p.add_argument("--workload", default="clustered4k",
                    choices=["clustered4k", "single", "divergent", "wide_trilinear"])
     p.add_argument("--seed", type=int, default=0)
@@ -150,24 +152,24 @@ def main():
         del src, dst
 
     # ---------------------------------------------------------------- headline
-    ev = []
+    # one event pair per timed step, made before the timed region
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
 
-    def step():
+    def step(i=None):
         ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders, bins=bins, stream=stream)
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
+        if i is not None:
+            ev[i][0].record(stream)
         ntc.decode(model, q, bins, out=out, stream=stream)
-        e1.record(stream)
-        ev.append((e0, e1))
+        if i is not None:
+            ev[i][1].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    ev.clear()
     t_start = time.perf_counter()
-    for _ in range(args.steps):
-        step()
+    for i in range(args.steps):
+        step(i)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     ms_step = wall * 1e3 / args.steps
@@ -271,7 +273,7 @@ def main():
                     ntc.decode(m, q, b, out=out, stream=stream)
                 else:
                     ntc.decode(m, q, None, out=out, stream=stream)
-            return timed(f, reps, 2, torch) * 1e3
+            return timed(f, reps, max(2, reps // 2), torch) * 1e3
 
         t = {f"d{w.n_decoders}_binned": ms_step,
              f"d{w.n_decoders}_stream": run(model, w.n_decoders, bins, False),

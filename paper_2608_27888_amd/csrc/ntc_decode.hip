@@ -164,7 +164,7 @@ __device__ void stage_decoder(const DecodeArgs &a, uint32_t dec, uint32_t *lds) 
       const uint16_t hb = p[off + (size_t)dout * din + row];
       v = (float)__builtin_bit_cast(_Float16, hb);
     }
-    bias[i] = v;
+    bias[i] = layer == n_layers - 1 ? v * -kLog2e : v;
   }
 }
 
@@ -418,8 +418,9 @@ __device__ __forceinline__ void relu_pack(const floatx16 &acc, half8 &s0, half8 
   s1 = as_half8(b);
 }
 
-__device__ __forceinline__ float sigmoid(float z) {
-  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-z * kLog2e));
+// 1 / (1 + exp(-(z + b))) with nb = -b * log2(e).
+__device__ __forceinline__ float sigmoid(float z, float nb) {
+  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(__builtin_fmaf(z, -kLog2e, nb)));
 }
 
 // Runs the staged decoder on the tile's features; returns the output layer's
@@ -471,8 +472,10 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
     frag += S::MB * S::KSH;
     bl += HID;
   }
-  // output layer: HID -> out (rows padded to 32 with zero weights and biases)
-  floatx16 c0 = bias_frag(bl, 0), c1 = c0;
+  // output layer: HID -> out (rows padded to 32 with zero weights).  Its
+  // accumulators start at zero (an inline constant); the bias is added by the
+  // sigmoid, which needs one multiply-add per value anyway.
+  floatx16 c0 = {}, c1 = {};
 #pragma unroll
   for (int s = 0; s < S::KSH; ++s) {
     const half8 w = a_frag(lds, frag + s);
@@ -481,6 +484,14 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
   }
   y0 = c0;
   y1 = c1;
+}
+
+// Output-layer biases of this lane's rows 4h..4h+3, pre-scaled by -log2(e)
+// when the decoder is staged (the sigmoid's exponent is then one fma).
+template <int NL, int CH, int HID, int NH>
+__device__ __forceinline__ floatx4 out_bias(const uint32_t *lds, int first_row) {
+  const float *b = (const float *)(lds) + image_of<NL, CH, HID>(NH).bias_off + HID * (1 + NH);
+  return *(const floatx4 *)(b + first_row + 4 * (lane_id() >> 5));
 }
 
 // Raw buffer resource over the output rows: a store whose byte offset lies past
@@ -495,31 +506,47 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_resource(const DecodeArgs 
   return __builtin_amdgcn_make_buffer_rsrc(a.out, 0, (int)bytes, 0x00020000);
 }
 
-// How a column block's rows reach memory: fp32 or fp16 runs of 4 rows (output
-// width a multiple of 4), or one store per row (any width, either format).
+// How a column block's rows reach memory: for an output width of 4 or 8, one
+// fp32 (or fp16) run of the 4 rows each lane holds; for any other width up to
+// 16, one store per row.
 enum StoreMode { kStoreF32x4 = 0, kStoreF16x4 = 1, kStoreEach = 2 };
 
 // Store instructions per 32-query column block; fixed for a mode, so the wait
 // counts of the software pipeline do not depend on the data.
 template <int STORE>
-constexpr int kStoresPerBlock = STORE == kStoreEach ? 8 : 2;
+constexpr int kStoresPerBlock = STORE == kStoreEach ? 8 : 1;
 
 // Decoded values this lane stores for one 32-query column block: rows 4h..4h+3
 // (lo) and 8+4h..8+4h+3 (hi) of the query in its column, after the sigmoid, as
-// fp32 bits.  The output width is <= 16; hi is computed only when the width
-// reaches it (otherwise its stores are dropped and its value is unused).
+// fp32 bits.  hi exists only in the per-row mode and is computed only when the
+// width reaches it (otherwise its stores are dropped and its value is unused).
 struct OutRows {
   u32x4 lo, hi;
 };
 
-__device__ __forceinline__ OutRows finish_rows(const floatx16 &z, int out_dim) {
+// Scaled output biases (see out_bias) of the lane's lo and hi rows.
+struct OutBias {
+  floatx4 lo, hi;
+};
+
+template <int NL, int CH, int HID, int NH, int STORE>
+__device__ __forceinline__ OutBias load_out_bias(const uint32_t *lds, int out_dim) {
+  OutBias b;
+  b.lo = out_bias<NL, CH, HID, NH>(lds, 0);
+  b.hi = STORE == kStoreEach && out_dim > 8 ? out_bias<NL, CH, HID, NH>(lds, 8) : b.lo;
+  return b;
+}
+
+template <int STORE>
+__device__ __forceinline__ OutRows finish_rows(const floatx16 &z, const OutBias &b, int out_dim) {
   OutRows r;
   r.hi = __builtin_nondeterministic_value(r.hi);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) r.lo[i] = __builtin_bit_cast(uint32_t, sigmoid(z[i]));
-  if (out_dim > 8) {
+  for (int i = 0; i < 4; ++i) r.lo[i] = __builtin_bit_cast(uint32_t, sigmoid(z[i], b.lo[i]));
+  if (STORE == kStoreEach && out_dim > 8) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) r.hi[i] = __builtin_bit_cast(uint32_t, sigmoid(z[4 + i]));
+    for (int i = 0; i < 4; ++i)
+      r.hi[i] = __builtin_bit_cast(uint32_t, sigmoid(z[4 + i], b.hi[i]));
   }
   return r;
 }
@@ -531,23 +558,19 @@ template <int STORE>
 __device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t out, int out_dim, uint32_t q,
                                            bool ok, const OutRows &r, uint32_t out_f16) {
   const int h = lane_id() >> 5;
-  const uint32_t row = q * (uint32_t)out_dim;
+  const int r0 = 4 * h;
   if constexpr (STORE == kStoreF32x4) {
-    const int r0 = 4 * h, r1 = 8 + 4 * h;
-    const uint32_t off0 = ok && r0 < out_dim ? (row + (uint32_t)r0) * 4u : kDropOffset;
-    const uint32_t off1 = ok && r1 < out_dim ? (row + (uint32_t)r1) * 4u : kDropOffset;
-    __builtin_amdgcn_raw_buffer_store_b128(r.lo, out, off0, 0, 0);
-    __builtin_amdgcn_raw_buffer_store_b128(r.hi, out, off1, 0, 0);
+    const uint32_t off = ok && r0 < out_dim ? (q * (uint32_t)out_dim + (uint32_t)r0) * 4u
+                                            : kDropOffset;
+    __builtin_amdgcn_raw_buffer_store_b128(r.lo, out, off, 0, 0);
   } else if constexpr (STORE == kStoreF16x4) {
-    const int r0 = 4 * h, r1 = 8 + 4 * h;
-    const uint32_t off0 = ok && r0 < out_dim ? (row + (uint32_t)r0) * 2u : kDropOffset;
-    const uint32_t off1 = ok && r1 < out_dim ? (row + (uint32_t)r1) * 2u : kDropOffset;
-    const float4 lo = __builtin_bit_cast(float4, r.lo), hi = __builtin_bit_cast(float4, r.hi);
+    const uint32_t off = ok && r0 < out_dim ? (q * (uint32_t)out_dim + (uint32_t)r0) * 2u
+                                            : kDropOffset;
+    const float4 lo = __builtin_bit_cast(float4, r.lo);
     const u32x2 lo16 = {pack_half2(lo.x, lo.y), pack_half2(lo.z, lo.w)};
-    const u32x2 hi16 = {pack_half2(hi.x, hi.y), pack_half2(hi.z, hi.w)};
-    __builtin_amdgcn_raw_buffer_store_b64(lo16, out, off0, 0, 0);
-    __builtin_amdgcn_raw_buffer_store_b64(hi16, out, off1, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b64(lo16, out, off, 0, 0);
   } else {
+    const uint32_t row = q * (uint32_t)out_dim;
     const uint32_t es = out_f16 ? 2u : 4u;
 #pragma unroll
     for (int g = 0; g < 2; ++g) {
@@ -570,15 +593,17 @@ __device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t out, int out_d
 // Column block 0 holds the queries of lanes 0..31, block 1 those of lanes
 // 32..63; a lane of half h stores, for each block, the query of lane
 // (block * 32 + lane % 32): its own in block h, its partner's in the other.
+// One v_permlane32_swap of (q, q) gives both: its first result holds the
+// lower half's values in both halves, its second the upper half's.
 template <int STORE>
 __device__ __forceinline__ void store_tile(__amdgpu_buffer_rsrc_t out, int out_dim, uint32_t q,
                                            bool ok, const OutRows &b0, const OutRows &b1,
                                            uint32_t out_f16) {
-  const uint32_t q_other = (uint32_t)__shfl_xor((int)q, 32, kWave);
-  const bool ok_other = __shfl_xor((int)ok, 32, kWave) != 0;
-  const bool h = lane_id() >= 32;
-  store_rows<STORE>(out, out_dim, h ? q_other : q, h ? ok_other : ok, b0, out_f16);
-  store_rows<STORE>(out, out_dim, h ? q : q_other, h ? ok : ok_other, b1, out_f16);
+  const uint32_t okw = ok ? 1u : 0u;
+  const auto qs = __builtin_amdgcn_permlane32_swap(q, q, false, false);
+  const auto oks = __builtin_amdgcn_permlane32_swap(okw, okw, false, false);
+  store_rows<STORE>(out, out_dim, qs[0], oks[0] != 0, b0, out_f16);
+  store_rows<STORE>(out, out_dim, qs[1], oks[1] != 0, b1, out_f16);
 }
 
 // Query data of a slot.  The loads are unconditional (a slot without a valid
@@ -739,8 +764,9 @@ decode_binned(const DecodeArgs a) {
     to_b_operands<S::KS0>(x, xb0, xb1);
     floatx16 z0, z1;
     run_mlp<NL, CH, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
-    const OutRows r0 = finish_rows(z0, a.out_dim);
-    const OutRows r1 = finish_rows(z1, a.out_dim);
+    const OutBias ob = load_out_bias<NL, CH, HID, NH, STORE>(lds, a.out_dim);
+    const OutRows r0 = finish_rows<STORE>(z0, ob, a.out_dim);
+    const OutRows r1 = finish_rows<STORE>(z1, ob, a.out_dim);
     __builtin_amdgcn_sched_barrier(0);
     // The next group's decoder is staged here, between this tile's MLP and the
     // next tile's fetches, so no fetched data is live across the staging.
@@ -825,8 +851,10 @@ decode_stream(const DecodeArgs a) {
       if (sel) {
         floatx16 z0, z1;
         run_mlp<NL, CH, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
-        store_tile<STORE>(out_rsrc, a.out_dim, q, mine_now, finish_rows(z0, a.out_dim),
-                          finish_rows(z1, a.out_dim), a.out_f16);
+        const OutBias ob = load_out_bias<NL, CH, HID, NH, STORE>(lds, a.out_dim);
+        store_tile<STORE>(out_rsrc, a.out_dim, q, mine_now,
+                          finish_rows<STORE>(z0, ob, a.out_dim),
+                          finish_rows<STORE>(z1, ob, a.out_dim), a.out_f16);
         todo &= ~sel;
         live = live && !mine_now;
       }
@@ -870,7 +898,8 @@ int launch_shape(const DecodeArgs &a, hipStream_t stream) {
 
 template <int NL, int CH, int HID, int NH, bool MIP, bool LEAKY>
 int launch_store(const DecodeArgs &a, hipStream_t stream) {
-  if (a.out_dim % 4 != 0) return launch_shape<NL, CH, HID, NH, MIP, kStoreEach, LEAKY>(a, stream);
+  if (a.out_dim != 4 && a.out_dim != 8)
+    return launch_shape<NL, CH, HID, NH, MIP, kStoreEach, LEAKY>(a, stream);
   return a.out_f16 ? launch_shape<NL, CH, HID, NH, MIP, kStoreF16x4, LEAKY>(a, stream)
                    : launch_shape<NL, CH, HID, NH, MIP, kStoreF32x4, LEAKY>(a, stream);
 }
