@@ -207,6 +207,33 @@ def main():
     e2e_bytes = decode_bytes + 12 * n
     e2e_roof_ms = max(e2e_bytes / (HBM_PEAK_GBS * 1e9), t_mfma) * 1e3
 
+    # ---------------------------------------------------------------- decoder variants
+    # The Sec. 4 setup's decoder (LeakyReLU, positional encoding, RGB rows) and
+    # its parts, on the same frame and bins: binned decode time of each.
+    variants = None
+    if not args.no_compare and w.mip is None:
+        # right after the headline (clocks settled), each with its own warm-up
+        reps = max(10, args.steps // 2)
+        variants = {}
+        for tag, ww, slope, dt in (
+                ("relu_f32x8", w, None, torch.float32),
+                ("leaky_f32x8", w, 0.01, torch.float32),
+                ("pe4_f32x8", w.with_pe(4, seed=args.seed), None, torch.float32),
+                ("f16x8", w, None, torch.float16),
+                ("sec4_setup_pe4_leaky_f16x3", w.with_pe(4, [0, 64, 64, 3], seed=args.seed), 0.01,
+                 torch.float16)):
+            # same latents, map and queries on the device; only the decoders differ
+            mv = model if ww is w else ntc.DeviceModel(
+                model.n_textures, model.res, model.channels, model.latents, ww.n_decoders,
+                list(ww.dims), torch.from_numpy(ww.params.view(np.int16)).to(dev),
+                model.tex_to_dec, ww.pe_octaves)
+            ov = torch.empty((n, ww.out_dim), dtype=dt, device=dev)
+            variants[tag] = round(timed(lambda: ntc.decode(mv, q, bins, out=ov, stream=stream,
+                                                          leaky_slope=slope, out_dtype=dt),
+                                        reps, reps, torch) * 1e3, 4)
+            del ov
+        log(f"[bench] decode variants {variants}")
+
     # ---------------------------------------------------------------- divergence
     per_s, tot_s = ntc.divergence_stats(q.tex_id, model.tex_to_dec, w.n_decoders)
     P = int(bins.bin_offset[-1].item())
@@ -242,6 +269,9 @@ def main():
                                    "divergence_metric_stream": round(divergence_metric(tot_s), 4),
                                    "divergence_metric_binned": round(divergence_metric(tot_b), 4)},
     }
+
+    if variants:
+        result["decode_variants_ms"] = variants
 
     # ---------------------------------------------------------------- divergence map (Sec. 2)
     if w.screen is not None:

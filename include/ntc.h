@@ -176,13 +176,23 @@ int ntc_decode(const ntc_grids *grids, const ntc_decoders *decoders,
 
 /*
  * Decoder variants of ntc_decode_ex.  The Sec. 4 setup trains its decoders with
- * LeakyReLU hidden activations and three output channels (RGB); fp16 output
- * rows halve the bytes the decode writes.
+ * LeakyReLU hidden activations, the encoder output concatenated with a
+ * positional encoding, and three output channels (RGB); fp16 output rows halve
+ * the bytes the decode writes.
+ *
+ * Positional encoding (the paper names it without its form; this is the
+ * library's reading): with K = pe_octaves, the decoder input is the latent
+ * feature vector followed by 4K values, for k = 0 .. K-1 in order
+ *   sin(2^k pi u), cos(2^k pi u), sin(2^k pi v), cos(2^k pi v)
+ * of the query's (u, v), so dims[0] = sum of channels + 4K.  K is 0 (none), 4
+ * or 8; K > 0 is supported for 2 levels of 8 or 16 channels, 3 layers of
+ * hidden width 64 and queries without mip (else NTC_ERR_UNSUPPORTED).
  */
 typedef struct {
   int32_t hidden_activation; /* NTC_ACT_RELU or NTC_ACT_LEAKY_RELU */
   float leaky_slope;         /* NTC_ACT_LEAKY_RELU only: 0 < slope < 1 (held as fp16) */
   int32_t output_format;     /* NTC_OUT_F32 or NTC_OUT_F16 */
+  int32_t pe_octaves;        /* positional-encoding octaves K: 0, 4 or 8 */
 } ntc_decode_options;
 
 /*

@@ -248,6 +248,22 @@ static void query_features(const uint16_t *tex_base, int32_t n_levels, const int
   }
 }
 
+/*
+ * Positional encoding of (u, v) with K octaves, appended to the decoder input
+ * (Sec. 4 setup: the encoder output is concatenated with a positional
+ * encoding; the paper does not give its form, this is the library's reading):
+ * for k = 0 .. K-1, sin(2^k pi u), cos(2^k pi u), sin(2^k pi v), cos(2^k pi v).
+ */
+static void pos_encoding(double u, double v, int K, double *x) {
+  for (int k = 0; k < K; ++k) {
+    const double a = ldexp(3.14159265358979323846, k); /* 2^k pi */
+    x[4 * k + 0] = sin(a * u);
+    x[4 * k + 1] = cos(a * u);
+    x[4 * k + 2] = sin(a * v);
+    x[4 * k + 3] = cos(a * v);
+  }
+}
+
 static void level_layout(int32_t n_levels, const int32_t *res, const int32_t *ch, size_t *off,
                          size_t *stride) {
   size_t acc = 0;
@@ -261,14 +277,17 @@ static void level_layout(int32_t n_levels, const int32_t *res, const int32_t *ch
 int ntc_oracle_features(const uint16_t *latents, int32_t n_textures, int32_t n_levels,
                         const int32_t *res, const int32_t *ch, const uint32_t *tex_id,
                         const float *uv, const float *mip, int64_t n, const int64_t *subset,
-                        int64_t n_sel, int32_t n_threads, double *out) {
-  if (!grids_valid(n_levels, res, ch, mip != NULL) || n < 0) return NTC_ORACLE_ERR_ARG;
+                        int64_t n_sel, int32_t n_threads, int32_t pe_octaves, double *out) {
+  if (!grids_valid(n_levels, res, ch, mip != NULL) || n < 0 || pe_octaves < 0 ||
+      pe_octaves > 16)
+    return NTC_ORACLE_ERR_ARG;
   if (!subset) n_sel = n;
   if (n_sel < 0 || (n_sel > 0 && (!latents || !tex_id || !uv || !out))) return NTC_ORACLE_ERR_ARG;
   size_t off[8], stride;
   level_layout(n_levels, res, ch, off, &stride);
-  int F = 0;
-  for (int l = 0; l < n_levels; ++l) F += ch[l];
+  int FL = 0;
+  for (int l = 0; l < n_levels; ++l) FL += ch[l];
+  const int F = FL + 4 * pe_octaves;
   int bad = 0;
 #pragma omp parallel for schedule(static) num_threads(n_threads > 0 ? n_threads : 1)
   for (int64_t i = 0; i < n_sel; ++i) {
@@ -279,6 +298,7 @@ int ntc_oracle_features(const uint16_t *latents, int32_t n_textures, int32_t n_l
     double scratch[256];
     query_features(latents + (size_t)t * stride, n_levels, res, ch, off, uv[2 * q],
                    uv[2 * q + 1], mip ? (double)mip[q] : 0.0, out + (size_t)i * F, scratch);
+    pos_encoding(uv[2 * q], uv[2 * q + 1], pe_octaves, out + (size_t)i * F + FL);
   }
   return bad ? NTC_ORACLE_ERR_ARG : NTC_ORACLE_OK;
 }
@@ -325,13 +345,14 @@ int ntc_oracle_decode(const uint16_t *latents, int32_t n_textures, int32_t n_lev
                       int32_t n_decoders, int32_t n_layers, const int32_t *dims,
                       const uint32_t *tex_to_dec, const uint32_t *tex_id, const float *uv,
                       const float *mip, int64_t n, const int64_t *subset, int64_t n_sel,
-                      int32_t n_threads, double leaky_slope, double *out) {
+                      int32_t n_threads, double leaky_slope, int32_t pe_octaves, double *out) {
   if (!grids_valid(n_levels, res, ch, mip != NULL) || !dims_valid(n_layers, dims) || n < 0 ||
-      n_decoders < 1 || !(leaky_slope >= 0.0 && leaky_slope < 1.0))
+      n_decoders < 1 || !(leaky_slope >= 0.0 && leaky_slope < 1.0) || pe_octaves < 0 ||
+      pe_octaves > 16)
     return NTC_ORACLE_ERR_ARG;
-  int F = 0;
-  for (int l = 0; l < n_levels; ++l) F += ch[l];
-  if (dims[0] != F) return NTC_ORACLE_ERR_ARG;
+  int FL = 0;
+  for (int l = 0; l < n_levels; ++l) FL += ch[l];
+  if (dims[0] != FL + 4 * pe_octaves) return NTC_ORACLE_ERR_ARG;
   if (!subset) n_sel = n;
   if (n_sel < 0 || (n_sel > 0 && (!latents || !params || !tex_to_dec || !tex_id || !uv || !out)))
     return NTC_ORACLE_ERR_ARG;
@@ -352,6 +373,7 @@ int ntc_oracle_decode(const uint16_t *latents, int32_t n_textures, int32_t n_lev
     double x[256], scratch[256];
     query_features(latents + (size_t)t * stride, n_levels, res, ch, off, uv[2 * q],
                    uv[2 * q + 1], mip ? (double)mip[q] : 0.0, x, scratch);
+    pos_encoding(uv[2 * q], uv[2 * q + 1], pe_octaves, x + FL);
     mlp(params + (size_t)d * dec_stride, n_layers, dims, x, leaky_slope,
         out + (size_t)i * out_dim);
   }

@@ -97,12 +97,15 @@ int ntc_oracle_divergence_map(const uint32_t *tex_id, int32_t width, int32_t hei
  * between adjacent pyramid levels by the query's mip; slots concatenated
  * finest first, channels in storage order.  out: [n_sel][sum(ch)].
  * subset: query indices to evaluate (NULL -> all n, n_sel = n).
+ * pe_octaves K >= 0 appends the positional encoding of (u, v) (Sec. 4 setup;
+ * its form is a reading): for k = 0 .. K-1, sin(2^k pi u), cos(2^k pi u),
+ * sin(2^k pi v), cos(2^k pi v).  Rows are [sum(ch) + 4K] wide.
  * Invalid queries (tex_id >= n_textures) leave their row untouched.
  */
 int ntc_oracle_features(const uint16_t *latents, int32_t n_textures, int32_t n_levels,
                         const int32_t *res, const int32_t *ch, const uint32_t *tex_id,
                         const float *uv, const float *mip, int64_t n, const int64_t *subset,
-                        int64_t n_sel, int32_t n_threads, double *out);
+                        int64_t n_sel, int32_t n_threads, int32_t pe_octaves, double *out);
 
 /*
  * Full decode: features as above, then the MLP of decoder tex_to_dec[tex_id[q]]:
@@ -111,6 +114,8 @@ int ntc_oracle_features(const uint16_t *latents, int32_t n_textures, int32_t n_l
  *   LeakyReLU for 0 < slope < 1); last layer logistic sigmoid.
  *   params: per decoder contiguous
  *   W0, b0, W1, b1, ... (fp16 bits).  out: [n_sel][dims[n_layers]].
+ *   The decoder input is the feature row with pe_octaves positional-encoding
+ *   octaves appended (dims[0] = sum(ch) + 4 * pe_octaves).
  * Invalid queries (bad tex_id or decoder id) leave their row untouched.
  */
 int ntc_oracle_decode(const uint16_t *latents, int32_t n_textures, int32_t n_levels,
@@ -118,7 +123,7 @@ int ntc_oracle_decode(const uint16_t *latents, int32_t n_textures, int32_t n_lev
                       int32_t n_decoders, int32_t n_layers, const int32_t *dims,
                       const uint32_t *tex_to_dec, const uint32_t *tex_id, const float *uv,
                       const float *mip, int64_t n, const int64_t *subset, int64_t n_sel,
-                      int32_t n_threads, double leaky_slope, double *out);
+                      int32_t n_threads, double leaky_slope, int32_t pe_octaves, double *out);
 
 /* fp16 bit pattern -> double (exact). */
 double ntc_oracle_half_to_double(uint16_t h);

@@ -45,9 +45,9 @@ def lib():
         L.ntc_oracle_divergence.argtypes = [P, i64, P, i32, i32, P, i64, i32, P, P]
         L.ntc_oracle_divergence_map.argtypes = [P, i32, i32, i32, P, i32, i32, i32, i32, P, P,
                                                 i32, P]
-        L.ntc_oracle_features.argtypes = [P, i32, i32, P, P, P, P, P, i64, P, i64, i32, P]
+        L.ntc_oracle_features.argtypes = [P, i32, i32, P, P, P, P, P, i64, P, i64, i32, i32, P]
         L.ntc_oracle_decode.argtypes = [P, i32, i32, P, P, P, i32, i32, P, P, P, P, P, i64, P,
-                                        i64, i32, ctypes.c_double, P]
+                                        i64, i32, ctypes.c_double, i32, P]
         L.ntc_oracle_half_to_double.argtypes = [ctypes.c_uint16]
         L.ntc_oracle_half_to_double.restype = ctypes.c_double
         for f in ("ntc_oracle_build_bins", "ntc_oracle_divergence", "ntc_oracle_divergence_map",
@@ -134,16 +134,19 @@ def _grid_args(w):
     return res, ch
 
 
-def features(w, subset=None, threads=None, fill=np.nan):
-    """Concatenated per-level latent samples of each query (rows of invalid queries = fill)."""
+def features(w, subset=None, threads=None, fill=np.nan, pe_octaves=None):
+    """Concatenated per-level latent samples of each query, followed by the
+    positional encoding when pe_octaves (default: the workload's) is > 0
+    (rows of invalid queries = fill)."""
     res, ch = _grid_args(w)
-    F = int(sum(w.channels))
+    K = int(getattr(w, "pe_octaves", 0) if pe_octaves is None else pe_octaves)
+    F = int(sum(w.channels)) + 4 * K
     sub = None if subset is None else np.ascontiguousarray(subset, dtype=np.int64)
     n_sel = w.n if sub is None else sub.shape[0]
     out = np.full((n_sel, F), fill, np.float64)
     rc = lib().ntc_oracle_features(_p(w.latents), w.n_textures, w.n_levels, _p(res), _p(ch),
                                    _p(w.tex_id), _p(w.uv), _p(w.mip), w.n, _p(sub), n_sel,
-                                   threads or default_threads(), _p(out))
+                                   threads or default_threads(), K, _p(out))
     if rc != 0:
         raise OracleError("ntc_oracle_features -> %d" % rc)
     return out
@@ -151,7 +154,8 @@ def features(w, subset=None, threads=None, fill=np.nan):
 
 def decode(w, subset=None, threads=None, fill=np.nan, leaky_slope=0.0):
     """Decoded channels of each query (rows of invalid queries = fill); hidden
-    activation ReLU, or LeakyReLU with 0 < leaky_slope < 1."""
+    activation ReLU, or LeakyReLU with 0 < leaky_slope < 1; the decoder input
+    carries the workload's positional-encoding octaves (w.pe_octaves)."""
     res, ch = _grid_args(w)
     dims = np.ascontiguousarray(w.dims, dtype=np.int32)
     sub = None if subset is None else np.ascontiguousarray(subset, dtype=np.int64)
@@ -161,7 +165,7 @@ def decode(w, subset=None, threads=None, fill=np.nan, leaky_slope=0.0):
                                  _p(w.params), w.n_decoders, w.n_layers, _p(dims),
                                  _p(w.tex_to_dec), _p(w.tex_id), _p(w.uv), _p(w.mip), w.n,
                                  _p(sub), n_sel, threads or default_threads(),
-                                 float(leaky_slope), _p(out))
+                                 float(leaky_slope), int(getattr(w, "pe_octaves", 0)), _p(out))
     if rc != 0:
         raise OracleError("ntc_oracle_decode -> %d" % rc)
     return out

@@ -73,13 +73,14 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
                   int64_t perm_capacity, int32_t align, const ntc_decode_options *opt,
                   void *out, void *stream) {
   if (!g || !m || !q) return NTC_ERR_ARG;
-  ntc_decode_options o = {NTC_ACT_RELU, 0.f, NTC_OUT_F32};
+  ntc_decode_options o = {NTC_ACT_RELU, 0.f, NTC_OUT_F32, 0};
   if (opt) o = *opt;
   if (o.hidden_activation != NTC_ACT_RELU && o.hidden_activation != NTC_ACT_LEAKY_RELU)
     return NTC_ERR_ARG;
   if (o.hidden_activation == NTC_ACT_LEAKY_RELU && !(o.leaky_slope > 0.f && o.leaky_slope < 1.f))
     return NTC_ERR_ARG;
   if (o.output_format != NTC_OUT_F32 && o.output_format != NTC_OUT_F16) return NTC_ERR_ARG;
+  if (o.pe_octaves != 0 && o.pe_octaves != 4 && o.pe_octaves != 8) return NTC_ERR_ARG;
   const int64_t elem = o.output_format == NTC_OUT_F16 ? 2 : 4;
   if (q->n < 0 || q->n > kMaxQueries) return NTC_ERR_ARG;
   if (g->n_textures < 1 || g->n_levels < 1 || g->n_levels > NTC_MAX_LEVELS) return NTC_ERR_ARG;
@@ -112,7 +113,7 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
     if (tex_stride >= ((int64_t)1 << 31)) return NTC_ERR_UNSUPPORTED;
   }
   // decoder shape: dims[0] = features, equal hidden widths, small output
-  const int F = L * ch;
+  const int F = L * ch + 4 * o.pe_octaves;
   const int nl = m->n_layers;
   if (m->dims[0] != F) return NTC_ERR_ARG;
   for (int i = 0; i <= nl; ++i)
@@ -151,6 +152,7 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
   const _Float16 slope = (_Float16)o.leaky_slope;
   a.slope_h2 = (uint32_t)__builtin_bit_cast(uint16_t, slope) * 0x00010001u;
   a.out_f16 = o.output_format == NTC_OUT_F16;
+  a.pe_octaves = o.pe_octaves;
   if (q->n == 0) return NTC_OK;
   return launch_decode(a, L, ch, F, hid, (hipStream_t)stream);
 }

@@ -64,15 +64,17 @@ __device__ __forceinline__ int sigma16(int k) {
   return (k & ~0xC) | ((k & 4) << 1) | ((k & 8) >> 1);
 }
 
-template <int NL, int CH, int HID>
+template <int NL, int CH, int PE, int HID>
 struct Shape {
-  static constexpr int F = NL * CH;          // features per query
+  static constexpr int FL = NL * CH;         // latent features per query
+  static constexpr int F = FL + PE;          // + positional-encoding features
   static constexpr int KS0 = F / 16;         // K-slices of layer 0
   static constexpr int MB = HID / 32;        // 32-row output blocks of a hidden layer
   static constexpr int KSH = HID / 16;       // K-slices of a layer fed by a hidden layer
   static_assert(F % 16 == 0, "feature count must be a multiple of 16");
   static_assert(HID % 32 == 0, "hidden width must be a multiple of 32");
   static_assert(CH == 8 || CH == 16, "8 or 16 channels per level");
+  static_assert(PE % 16 == 0, "positional features come in whole K-slices");
 };
 
 // LDS image of one decoder: A fragments (64 lanes x 16 B each), then fp32
@@ -84,9 +86,9 @@ struct Image {
   int bytes;
 };
 
-template <int NL, int CH, int HID>
+template <int NL, int CH, int PE, int HID>
 __host__ __device__ inline Image image_of(int n_hidden) {
-  using S = Shape<NL, CH, HID>;
+  using S = Shape<NL, CH, PE, HID>;
   Image im;
   im.n_frags = S::MB * S::KS0 + n_hidden * S::MB * S::KSH + S::KSH;
   im.bias_off = im.n_frags * 256;  // 1024 B = 256 floats per fragment
@@ -97,10 +99,10 @@ __host__ __device__ inline Image image_of(int n_hidden) {
 
 // Copies decoder `dec` into the LDS image, re-arranged into A fragments; all
 // threads of the workgroup take part; the caller brackets it with barriers.
-template <int NL, int CH, int HID, int THREADS>
+template <int NL, int CH, int PE, int HID, int THREADS>
 __device__ void stage_decoder(const DecodeArgs &a, uint32_t dec, uint32_t *lds) {
-  using S = Shape<NL, CH, HID>;
-  const Image im = image_of<NL, CH, HID>(a.n_hidden);
+  using S = Shape<NL, CH, PE, HID>;
+  const Image im = image_of<NL, CH, PE, HID>(a.n_hidden);
   const uint16_t *p = a.params + (size_t)dec * (size_t)a.dec_stride;
   const int n_layers = a.n_hidden + 2;
   // fragment lane-slices: one 16-byte lane slice per iteration
@@ -185,6 +187,23 @@ __device__ __forceinline__ floatx16 bias_frag(const float *bias_layer, int mb) {
 
 __device__ __forceinline__ half8 a_frag(const uint32_t *lds, int f) {
   return as_half8(*(const u32x4 *)(lds + (size_t)f * 256 + lane_id() * 4));
+}
+
+// Positional encoding of the query's texture coordinate, PE / 4 octaves k:
+// sin(2^k pi u), cos(2^k pi u), sin(2^k pi v), cos(2^k pi v), appended after
+// the latent features as fp16 pairs (sin, cos).  v_sin_f32 / v_cos_f32 take
+// the angle in turns: 2^k pi u is 2^(k-1) u turns, reduced to [0, 1) first
+// (exact in fp32) so any finite coordinate stays inside the instructions'
+// input range.
+template <int PE>
+__device__ __forceinline__ void pos_encoding(float u, float v, uint32_t *xo) {
+#pragma unroll
+  for (int k = 0; k < PE / 4; ++k) {
+    const float scale = k == 0 ? 0.5f : (float)(1 << (k - 1));
+    const float tu = __builtin_amdgcn_fractf(u * scale), tv = __builtin_amdgcn_fractf(v * scale);
+    xo[2 * k] = pack_half2(__builtin_amdgcn_sinf(tu), __builtin_amdgcn_cosf(tu));
+    xo[2 * k + 1] = pack_half2(__builtin_amdgcn_sinf(tv), __builtin_amdgcn_cosf(tv));
+  }
 }
 
 // -------------------------------------------------------------------- gather
@@ -303,9 +322,10 @@ __device__ __forceinline__ T pick(const T (&v)[NTC_MAX_LEVELS], int k) {
 
 // Feature vector of the lane's query, packed as fp16 pairs: x[c/2] holds
 // features c and c+1; slot l occupies features [l*CH, (l+1)*CH).
-template <int NL, int CH, bool MIP>
+template <int NL, int CH, int PE, bool MIP>
 __device__ __forceinline__ void gather(const DecodeArgs &a, const Query &qq,
-                                       uint32_t (&x)[NL * CH / 2]) {
+                                       uint32_t (&x)[(NL * CH + PE) / 2]) {
+  if constexpr (PE > 0) pos_encoding<PE>(qq.u, qq.v, x + NL * CH / 2);
   const uint16_t *tex = a.latents + (size_t)qq.tex * (size_t)a.tex_stride;
 #pragma unroll
   for (int l = 0; l < NL; ++l) {
@@ -350,9 +370,9 @@ __device__ __forceinline__ void fetch_taps(const DecodeArgs &a, const Query &qq,
     fetch_level<CH>(tex, a.level_off[l], a.res[l], a.resf[l], qq.u, qq.v, T.lv[l]);
 }
 
-template <int NL, int CH>
+template <int NL, int CH, int PE>
 __device__ __forceinline__ void interp_taps(const TileTaps<NL, CH> &T,
-                                            uint32_t (&x)[NL * CH / 2]) {
+                                            uint32_t (&x)[(NL * CH + PE) / 2]) {
 #pragma unroll
   for (int l = 0; l < NL; ++l) interp_level_h2<CH>(T.lv[l], x + l * CH / 2);
 }
@@ -425,13 +445,13 @@ __device__ __forceinline__ float sigmoid(float z, float nb) {
 
 // Runs the staged decoder on the tile's features; returns the output layer's
 // accumulators (sigmoid applied) for the two column blocks.
-template <int NL, int CH, int HID, int NH, bool LEAKY>
+template <int NL, int CH, int PE, int HID, int NH, bool LEAKY>
 __device__ __forceinline__ void run_mlp(const uint32_t *lds,
-                                        const half8 (&xb0)[NL * CH / 16],
-                                        const half8 (&xb1)[NL * CH / 16], floatx16 &y0,
+                                        const half8 (&xb0)[(NL * CH + PE) / 16],
+                                        const half8 (&xb1)[(NL * CH + PE) / 16], floatx16 &y0,
                                         floatx16 &y1, uint32_t slope_h2) {
-  using S = Shape<NL, CH, HID>;
-  const float *bias = (const float *)(lds) + image_of<NL, CH, HID>(NH).bias_off;
+  using S = Shape<NL, CH, PE, HID>;
+  const float *bias = (const float *)(lds) + image_of<NL, CH, PE, HID>(NH).bias_off;
   half8 h0[S::KSH], h1[S::KSH];
   // layer 0: F -> HID
 #pragma unroll
@@ -488,9 +508,9 @@ __device__ __forceinline__ void run_mlp(const uint32_t *lds,
 
 // Output-layer biases of this lane's rows 4h..4h+3, pre-scaled by -log2(e)
 // when the decoder is staged (the sigmoid's exponent is then one fma).
-template <int NL, int CH, int HID, int NH>
+template <int NL, int CH, int PE, int HID, int NH>
 __device__ __forceinline__ floatx4 out_bias(const uint32_t *lds, int first_row) {
-  const float *b = (const float *)(lds) + image_of<NL, CH, HID>(NH).bias_off + HID * (1 + NH);
+  const float *b = (const float *)(lds) + image_of<NL, CH, PE, HID>(NH).bias_off + HID * (1 + NH);
   return *(const floatx4 *)(b + first_row + 4 * (lane_id() >> 5));
 }
 
@@ -529,11 +549,11 @@ struct OutBias {
   floatx4 lo, hi;
 };
 
-template <int NL, int CH, int HID, int NH, int STORE>
+template <int NL, int CH, int PE, int HID, int NH, int STORE>
 __device__ __forceinline__ OutBias load_out_bias(const uint32_t *lds, int out_dim) {
   OutBias b;
-  b.lo = out_bias<NL, CH, HID, NH>(lds, 0);
-  b.hi = STORE == kStoreEach && out_dim > 8 ? out_bias<NL, CH, HID, NH>(lds, 8) : b.lo;
+  b.lo = out_bias<NL, CH, PE, HID, NH>(lds, 0);
+  b.hi = STORE == kStoreEach && out_dim > 8 ? out_bias<NL, CH, PE, HID, NH>(lds, 8) : b.lo;
   return b;
 }
 
@@ -686,11 +706,11 @@ constexpr int kThreads = kWaves<HID> * kWave;
 template <int HID>
 constexpr int kMinBlocks = HID <= 64 ? 4 : 1;
 
-template <int NL, int CH, int HID, int NH, bool MIP, int STORE, bool LEAKY>
+template <int NL, int CH, int PE, int HID, int NH, bool MIP, int STORE, bool LEAKY>
 __global__ void __launch_bounds__(kThreads<HID>, kMinBlocks<HID>)
 decode_binned(const DecodeArgs a) {
   constexpr int WAVES = kWaves<HID>;
-  using S = Shape<NL, CH, HID>;
+  using S = Shape<NL, CH, PE, HID>;
   extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
   const uint32_t w = threadIdx.x / kWave, lane = lane_id();
   const uint32_t D = (uint32_t)a.n_decoders;
@@ -736,7 +756,7 @@ decode_binned(const DecodeArgs a) {
   // prefetch has a whole tile of work to land.
   auto restage = [&](uint32_t d) {
     __syncthreads();  // every wave is done with the previous decoder
-    stage_decoder<NL, CH, HID, kThreads<HID>>(a, d, lds);
+    stage_decoder<NL, CH, PE, HID, kThreads<HID>>(a, d, lds);
     __syncthreads();
   };
   const Slot s0 = slot_query(g0);
@@ -764,14 +784,16 @@ decode_binned(const DecodeArgs a) {
   auto tile = [&](const Query &q_in, const Slot &p_in, Query &q_out, Slot &p_out) {
     uint32_t x[S::F / 2];
     if constexpr (MIP)
-      gather<NL, CH, MIP>(a, cur, x);
-    else
-      interp_taps<NL, CH>(taps, x);
+      gather<NL, CH, PE, MIP>(a, cur, x);
+    else {
+      interp_taps<NL, CH, PE>(taps, x);
+      if constexpr (PE > 0) pos_encoding<PE>(cur.u, cur.v, x + NL * CH / 2);
+    }
     half8 xb0[S::KS0], xb1[S::KS0];
     to_b_operands<S::KS0>(x, xb0, xb1);
     floatx16 z0, z1;
-    run_mlp<NL, CH, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
-    const OutBias ob = load_out_bias<NL, CH, HID, NH, STORE>(lds, a.out_dim);
+    run_mlp<NL, CH, PE, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
+    const OutBias ob = load_out_bias<NL, CH, PE, HID, NH, STORE>(lds, a.out_dim);
     const OutRows r0 = finish_rows<STORE>(z0, ob, a.out_dim);
     const OutRows r1 = finish_rows<STORE>(z1, ob, a.out_dim);
     __builtin_amdgcn_sched_barrier(0);
@@ -807,11 +829,11 @@ decode_binned(const DecodeArgs a) {
   }
 }
 
-template <int NL, int CH, int HID, int NH, bool MIP, int STORE, bool LEAKY>
+template <int NL, int CH, int PE, int HID, int NH, bool MIP, int STORE, bool LEAKY>
 __global__ void __launch_bounds__(kThreads<HID>, kMinBlocks<HID>)
 decode_stream(const DecodeArgs a) {
   constexpr int WAVES = kWaves<HID>;
-  using S = Shape<NL, CH, HID>;
+  using S = Shape<NL, CH, PE, HID>;
   extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
   __shared__ uint32_t next_dec[2][WAVES];
   const uint32_t w = threadIdx.x / kWave, lane = lane_id();
@@ -834,7 +856,7 @@ decode_stream(const DecodeArgs a) {
       dq = live ? dd : 0xFFFFFFFFu;
     }
     uint32_t x[S::F / 2];
-    gather<NL, CH, MIP>(a, qq, x);
+    gather<NL, CH, PE, MIP>(a, qq, x);
     half8 xb0[S::KS0], xb1[S::KS0];
     to_b_operands<S::KS0>(x, xb0, xb1);
     uint64_t todo = ballot(live);
@@ -849,7 +871,7 @@ decode_stream(const DecodeArgs a) {
       parity ^= 1;
       if (d == 0xFFFFFFFFu) break;
       if (d != staged) {
-        stage_decoder<NL, CH, HID, kThreads<HID>>(a, d, lds);
+        stage_decoder<NL, CH, PE, HID, kThreads<HID>>(a, d, lds);
         __syncthreads();
         staged = d;
       }
@@ -857,8 +879,8 @@ decode_stream(const DecodeArgs a) {
       const uint64_t sel = ballot(mine_now);
       if (sel) {
         floatx16 z0, z1;
-        run_mlp<NL, CH, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
-        const OutBias ob = load_out_bias<NL, CH, HID, NH, STORE>(lds, a.out_dim);
+        run_mlp<NL, CH, PE, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
+        const OutBias ob = load_out_bias<NL, CH, PE, HID, NH, STORE>(lds, a.out_dim);
         store_tile<STORE>(out_rsrc, a.out_dim, q, mine_now,
                           finish_rows<STORE>(z0, ob, a.out_dim),
                           finish_rows<STORE>(z1, ob, a.out_dim), a.out_f16);
@@ -869,15 +891,15 @@ decode_stream(const DecodeArgs a) {
   }
 }
 
-template <int NL, int CH, int HID, int NH, bool MIP, int STORE, bool LEAKY>
+template <int NL, int CH, int PE, int HID, int NH, bool MIP, int STORE, bool LEAKY>
 int launch_shape(const DecodeArgs &a, hipStream_t stream) {
-  const Image im = image_of<NL, CH, HID>(NH);
+  const Image im = image_of<NL, CH, PE, HID>(NH);
   const size_t lds = (size_t)im.bytes;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess)
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  const void *fn = a.bin_offset ? (const void *)decode_binned<NL, CH, HID, NH, MIP, STORE, LEAKY>
-                                : (const void *)decode_stream<NL, CH, HID, NH, MIP, STORE, LEAKY>;
+  const void *fn = a.bin_offset ? (const void *)decode_binned<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>
+                                : (const void *)decode_stream<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>;
   if (lds > 64 * 1024) {
     if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
         hipSuccess)
@@ -895,39 +917,47 @@ int launch_shape(const DecodeArgs &a, hipStream_t stream) {
   if (blocks > cap) blocks = cap;
   if (blocks == 0) return NTC_OK;
   if (a.bin_offset)
-    hipLaunchKernelGGL((decode_binned<NL, CH, HID, NH, MIP, STORE, LEAKY>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((decode_binned<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>), dim3((unsigned)blocks),
                        dim3(threads), lds, stream, a);
   else
-    hipLaunchKernelGGL((decode_stream<NL, CH, HID, NH, MIP, STORE, LEAKY>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((decode_stream<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>), dim3((unsigned)blocks),
                        dim3(threads), lds, stream, a);
   return hip_status(hipGetLastError());
 }
 
-template <int NL, int CH, int HID, int NH, bool MIP, bool LEAKY>
+template <int NL, int CH, int PE, int HID, int NH, bool MIP, bool LEAKY>
 int launch_store(const DecodeArgs &a, hipStream_t stream) {
   if (a.out_dim != 4 && a.out_dim != 8)
-    return launch_shape<NL, CH, HID, NH, MIP, kStoreEach, LEAKY>(a, stream);
-  return a.out_f16 ? launch_shape<NL, CH, HID, NH, MIP, kStoreF16x4, LEAKY>(a, stream)
-                   : launch_shape<NL, CH, HID, NH, MIP, kStoreF32x4, LEAKY>(a, stream);
+    return launch_shape<NL, CH, PE, HID, NH, MIP, kStoreEach, LEAKY>(a, stream);
+  return a.out_f16 ? launch_shape<NL, CH, PE, HID, NH, MIP, kStoreF16x4, LEAKY>(a, stream)
+                   : launch_shape<NL, CH, PE, HID, NH, MIP, kStoreF32x4, LEAKY>(a, stream);
 }
 
-template <int NL, int CH, int HID, int NH, bool MIP>
+template <int NL, int CH, int PE, int HID, int NH, bool MIP>
 int launch_act(const DecodeArgs &a, hipStream_t stream) {
-  return a.leaky ? launch_store<NL, CH, HID, NH, MIP, true>(a, stream)
-                 : launch_store<NL, CH, HID, NH, MIP, false>(a, stream);
+  return a.leaky ? launch_store<NL, CH, PE, HID, NH, MIP, true>(a, stream)
+                 : launch_store<NL, CH, PE, HID, NH, MIP, false>(a, stream);
 }
 
-template <int NL, int CH, int HID, int NH>
+// Positional-encoding kernels exist for the Sec. 4 setup's decoder only: one
+// hidden -> hidden layer, no mip blending.
+template <int NL, int CH, int PE, int HID, int NH>
 int launch_mip(const DecodeArgs &a, hipStream_t stream) {
-  return a.mip ? launch_act<NL, CH, HID, NH, true>(a, stream)
-               : launch_act<NL, CH, HID, NH, false>(a, stream);
+  if constexpr (PE > 0) {
+    return a.mip ? NTC_ERR_UNSUPPORTED : launch_act<NL, CH, PE, HID, NH, false>(a, stream);
+  } else {
+    return a.mip ? launch_act<NL, CH, PE, HID, NH, true>(a, stream)
+                 : launch_act<NL, CH, PE, HID, NH, false>(a, stream);
+  }
 }
 
-template <int NL, int CH, int HID>
+template <int NL, int CH, int PE, int HID>
 int launch_hidden(const DecodeArgs &a, hipStream_t stream) {
   switch (a.n_hidden) {
-    case 1: return launch_mip<NL, CH, HID, 1>(a, stream);
-    case 2: return launch_mip<NL, CH, HID, 2>(a, stream);
+    case 1: return launch_mip<NL, CH, PE, HID, 1>(a, stream);
+    case 2:
+      if constexpr (PE > 0) return NTC_ERR_UNSUPPORTED;
+      else return launch_mip<NL, CH, PE, HID, 2>(a, stream);
     default: return NTC_ERR_UNSUPPORTED;
   }
 }
@@ -937,14 +967,21 @@ int launch_hidden(const DecodeArgs &a, hipStream_t stream) {
 int launch_decode(const DecodeArgs &a, int n_levels, int channels, int feat, int hidden,
                   hipStream_t stream) {
   (void)feat;
-  if (hidden == 64) {
-    if (n_levels == 2 && channels == 8) return launch_hidden<2, 8, 64>(a, stream);
-    if (n_levels == 2 && channels == 16) return launch_hidden<2, 16, 64>(a, stream);
-    if (n_levels == 3 && channels == 16) return launch_hidden<3, 16, 64>(a, stream);
-  } else if (hidden == 128) {
-    if (n_levels == 2 && channels == 8) return launch_hidden<2, 8, 128>(a, stream);
-    if (n_levels == 2 && channels == 16) return launch_hidden<2, 16, 128>(a, stream);
-    if (n_levels == 3 && channels == 16) return launch_hidden<3, 16, 128>(a, stream);
+  if (a.pe_octaves == 0) {
+    if (hidden == 64) {
+      if (n_levels == 2 && channels == 8) return launch_hidden<2, 8, 0, 64>(a, stream);
+      if (n_levels == 2 && channels == 16) return launch_hidden<2, 16, 0, 64>(a, stream);
+      if (n_levels == 3 && channels == 16) return launch_hidden<3, 16, 0, 64>(a, stream);
+    } else if (hidden == 128) {
+      if (n_levels == 2 && channels == 8) return launch_hidden<2, 8, 0, 128>(a, stream);
+      if (n_levels == 2 && channels == 16) return launch_hidden<2, 16, 0, 128>(a, stream);
+      if (n_levels == 3 && channels == 16) return launch_hidden<3, 16, 0, 128>(a, stream);
+    }
+  } else if (hidden == 64 && n_levels == 2) {
+    if (channels == 8 && a.pe_octaves == 4) return launch_hidden<2, 8, 16, 64>(a, stream);
+    if (channels == 8 && a.pe_octaves == 8) return launch_hidden<2, 8, 32, 64>(a, stream);
+    if (channels == 16 && a.pe_octaves == 4) return launch_hidden<2, 16, 16, 64>(a, stream);
+    if (channels == 16 && a.pe_octaves == 8) return launch_hidden<2, 16, 32, 64>(a, stream);
   }
   return NTC_ERR_UNSUPPORTED;
 }

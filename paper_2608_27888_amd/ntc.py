@@ -183,6 +183,7 @@ class DeviceModel:
     dims: list
     params: torch.Tensor       # int16 view of fp16 bits
     tex_to_dec: torch.Tensor   # int32 view of uint32
+    pe_octaves: int = 0        # positional-encoding octaves of the decoder input
 
     def grids(self) -> Grids:
         g = Grids()
@@ -235,7 +236,8 @@ def upload(w, device="cuda"):
     """Host workload (paper_2608_27888_amd.workloads.Workload) -> (DeviceModel, DeviceQueries)."""
     model = DeviceModel(w.n_textures, list(w.res), list(w.channels),
                         _dev(w.latents, np.int16, device), w.n_decoders, list(w.dims),
-                        _dev(w.params, np.int16, device), _dev(w.tex_to_dec, np.int32, device))
+                        _dev(w.params, np.int16, device), _dev(w.tex_to_dec, np.int32, device),
+                        int(getattr(w, "pe_octaves", 0)))
     queries = DeviceQueries(_dev(w.tex_id, np.int32, device), _dev(w.uv, np.float32, device),
                             None if w.mip is None else _dev(w.mip, np.float32, device))
     return model, queries
@@ -247,7 +249,7 @@ NTC_OUT_F32, NTC_OUT_F16 = 0, 1
 
 class DecodeOptions(ctypes.Structure):
     _fields_ = [("hidden_activation", ctypes.c_int32), ("leaky_slope", ctypes.c_float),
-                ("output_format", ctypes.c_int32)]
+                ("output_format", ctypes.c_int32), ("pe_octaves", ctypes.c_int32)]
 
 
 def decode(model: DeviceModel, queries: DeviceQueries, bins: Optional[Bins] = None,
@@ -255,7 +257,8 @@ def decode(model: DeviceModel, queries: DeviceQueries, bins: Optional[Bins] = No
            out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
     """Binned mode when `bins` is given, stream (divergent) mode otherwise.  Hidden
     activation ReLU, or LeakyReLU max(x, slope x) when leaky_slope is given; output
-    rows float32 or float16."""
+    rows float32 or float16; the model's positional-encoding octaves extend the
+    decoder input."""
     if out_dtype not in (torch.float32, torch.float16):
         raise ValueError("out_dtype must be float32 or float16")
     if out is None:
@@ -266,7 +269,8 @@ def decode(model: DeviceModel, queries: DeviceQueries, bins: Optional[Bins] = No
     g, d, q = model.grids(), model.decoders(), queries.struct()
     opt = DecodeOptions(NTC_ACT_RELU if leaky_slope is None else NTC_ACT_LEAKY_RELU,
                         0.0 if leaky_slope is None else float(leaky_slope),
-                        NTC_OUT_F16 if out_dtype == torch.float16 else NTC_OUT_F32)
+                        NTC_OUT_F16 if out_dtype == torch.float16 else NTC_OUT_F32,
+                        int(model.pe_octaves))
     if bins is not None:
         st = lib().ntc_decode_ex(ctypes.byref(g), ctypes.byref(d), _ptr(model.tex_to_dec),
                                  ctypes.byref(q), _ptr(bins.bin_offset), _ptr(bins.perm),

@@ -59,6 +59,7 @@ class Workload:
     mip: Optional[np.ndarray]    # float32 [N] or None (=> 0)
     screen: Optional[tuple] = None  # (width, height, samples per pixel)
     meta: dict = field(default_factory=dict)
+    pe_octaves: int = 0          # positional-encoding octaves of the decoder input
 
     @property
     def n(self) -> int:
@@ -96,7 +97,20 @@ class Workload:
         return Workload(f"{self.name}_mlp{'-'.join(map(str, dims))}", self.n_textures,
                         list(self.res), list(self.channels), self.latents, self.n_decoders,
                         list(dims), params, self.tex_to_dec, self.tex_id, self.uv, self.mip,
-                        self.screen, dict(self.meta))
+                        self.screen, dict(self.meta), self.pe_octaves)
+
+    def with_pe(self, octaves: int, dims=None, seed: int = 0) -> "Workload":
+        """Same grids, map and queries; decoders redrawn for an input of the
+        latent features followed by `octaves` positional-encoding octaves
+        (dims[0] = sum(channels) + 4 * octaves; the other widths as given, or
+        the workload's)."""
+        d0 = int(sum(self.channels)) + 4 * int(octaves)
+        dims = [d0] + list(self.dims[1:] if dims is None else dims[1:])
+        params = draw_decoders(seed, self.n_decoders, dims)
+        return Workload(f"{self.name}_pe{octaves}", self.n_textures, list(self.res),
+                        list(self.channels), self.latents, self.n_decoders, dims, params,
+                        self.tex_to_dec, self.tex_id, self.uv, self.mip, self.screen,
+                        dict(self.meta), int(octaves))
 
     def with_decoders(self, n_decoders: int, tex_to_dec: np.ndarray, seed: int = 0,
                       name: Optional[str] = None) -> "Workload":
@@ -105,7 +119,7 @@ class Workload:
         return Workload(name or f"{self.name}_d{n_decoders}", self.n_textures, list(self.res),
                         list(self.channels), self.latents, n_decoders, list(self.dims), params,
                         np.ascontiguousarray(tex_to_dec, dtype=np.uint32), self.tex_id, self.uv,
-                        self.mip, self.screen, dict(self.meta))
+                        self.mip, self.screen, dict(self.meta), self.pe_octaves)
 
 
 def texture_stride(res, channels) -> int:

@@ -13,6 +13,12 @@ HEADER = os.path.join(ROOT, "include", "ntc.h")
 
 FAKE = ctypes.c_void_p(0x100000)  # never dereferenced: validation fails first
 
+# A call that passes validation goes on to launch kernels on FAKE pointers.  That
+# only happens here without a device (the launch then fails with NTC_ERR_HIP);
+# with a device those checks are skipped.  Counting devices does not initialise
+# them.
+HAS_DEVICE = __import__("torch").cuda.device_count() > 0
+
 
 def declared_functions():
     text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
@@ -105,9 +111,10 @@ def test_decode_validation(L):
     assert _decode(L, dims=(32, 64, 48, 8)) == ntc.NTC_ERR_UNSUPPORTED  # unequal hidden widths
     assert _decode(L, dims=(32, 96, 96, 8)) == ntc.NTC_ERR_UNSUPPORTED  # width not built
     assert _decode(L, dims=(32, 64, 64, 20)) == ntc.NTC_ERR_UNSUPPORTED  # too many outputs
-    assert _decode(L, dims=(32, 64, 64, 3)) != ntc.NTC_ERR_UNSUPPORTED   # RGB rows are built
     assert _decode(L, n=1 << 27, dims=(32, 64, 64, 8)) == ntc.NTC_ERR_UNSUPPORTED  # > 4 GiB
-    assert _decode(L, n=(1 << 27) - 16, dims=(32, 64, 64, 4)) != ntc.NTC_ERR_UNSUPPORTED  # 2 GiB
+    if not HAS_DEVICE:
+        assert _decode(L, dims=(32, 64, 64, 3)) == ntc.NTC_ERR_HIP   # RGB rows are built
+        assert _decode(L, n=(1 << 27) - 16, dims=(32, 64, 64, 4)) == ntc.NTC_ERR_HIP  # 2 GiB
     assert _decode(L, dims=(32, 8)) == ntc.NTC_ERR_UNSUPPORTED          # no hidden layer
     assert _decode(L, res=(256, 128), ch=(16, 8), dims=(24, 64, 8)) == ntc.NTC_ERR_UNSUPPORTED
     assert _decode(L, res=(0, 128)) == ntc.NTC_ERR_ARG
@@ -161,8 +168,8 @@ def test_decode_options_validation(L):
     q = ntc.Queries()
     q.tex_id, q.uv, q.mip, q.n = FAKE, FAKE, None, 100
 
-    def call(act, slope, fmt):
-        o = ntc.DecodeOptions(act, slope, fmt)
+    def call(act, slope, fmt, pe=0):
+        o = ntc.DecodeOptions(act, slope, fmt, pe)
         return L.ntc_decode_ex(ctypes.byref(g), ctypes.byref(d), FAKE, ctypes.byref(q), None,
                                None, 0, 0, ctypes.byref(o), FAKE, None)
 
@@ -170,4 +177,17 @@ def test_decode_options_validation(L):
     assert call(ntc.NTC_ACT_LEAKY_RELU, 0.0, 0) == ntc.NTC_ERR_ARG
     assert call(ntc.NTC_ACT_LEAKY_RELU, 1.0, 0) == ntc.NTC_ERR_ARG
     assert call(ntc.NTC_ACT_RELU, 0.0, 2) == ntc.NTC_ERR_ARG  # unknown output format
-    assert call(ntc.NTC_ACT_LEAKY_RELU, 0.01, ntc.NTC_OUT_F16) != ntc.NTC_ERR_ARG
+    if not HAS_DEVICE:
+        assert call(ntc.NTC_ACT_LEAKY_RELU, 0.01, ntc.NTC_OUT_F16) == ntc.NTC_ERR_HIP
+    # positional encoding: 0, 4 or 8 octaves; dims[0] must include its 4K values
+    assert call(ntc.NTC_ACT_RELU, 0.0, 0, pe=3) == ntc.NTC_ERR_ARG
+    assert call(ntc.NTC_ACT_RELU, 0.0, 0, pe=-4) == ntc.NTC_ERR_ARG
+    assert call(ntc.NTC_ACT_RELU, 0.0, 0, pe=4) == ntc.NTC_ERR_ARG   # dims[0] is still 32
+    d.dims[0] = 48
+    if not HAS_DEVICE:
+        assert call(ntc.NTC_ACT_LEAKY_RELU, 0.01, 0, pe=4) == ntc.NTC_ERR_HIP  # built: launches
+    assert call(ntc.NTC_ACT_RELU, 0.0, 0, pe=8) == ntc.NTC_ERR_ARG   # 32 + 32 != 48
+    d.n_layers = 4
+    for i, v in enumerate((48, 64, 64, 64, 8)):
+        d.dims[i] = v
+    assert call(ntc.NTC_ACT_RELU, 0.0, 0, pe=4) == ntc.NTC_ERR_UNSUPPORTED  # two hidden->hidden

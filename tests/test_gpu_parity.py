@@ -285,3 +285,33 @@ def test_decode_texel_centres_and_far_uv(dev, oracle):
     model, q = ntc.upload(w, dev)
     out = ntc.decode(model, q).cpu().numpy()
     assert np.abs(out - oracle.decode(w)).max() <= TOL
+
+
+@pytest.mark.parametrize("name,octaves,dims,slope,dtype", [
+    ("clustered4k", 4, None, None, torch.float32),
+    ("clustered4k", 8, None, 0.01, torch.float32),
+    ("clustered4k", 4, [48, 64, 64, 3], 0.01, torch.float16),  # the Sec. 4 setup's decoder
+    ("tiny", 4, None, None, torch.float32),
+    ("tiny", 8, [48, 64, 64, 3], 0.01, torch.float32),
+    ("single", 4, None, 0.05, torch.float32),
+])
+def test_decode_positional_encoding(dev, oracle, name, octaves, dims, slope, dtype):
+    """Decoder input = latent features + positional encoding of (u, v) (Sec. 4
+    setup), binned and stream order, against the oracle; a few queries far
+    outside [0, 1) exercise the angle reduction."""
+    w = small(name).with_pe(octaves, dims, seed=7)
+    w.uv = w.uv.copy()
+    w.uv[5::97] = np.array([[1000.3, -3.7e5]], np.float32)
+    w.uv[11::131] = np.array([[-17.25, 2.0e6]], np.float32)
+    say(f"[pe] {name} octaves={octaves} dims={w.dims} slope={slope} {dtype} n={w.n}")
+    model, q = ntc.upload(w, dev)
+    assert model.pe_octaves == octaves
+    bins = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders)
+    out_b = ntc.decode(model, q, bins, leaky_slope=slope, out_dtype=dtype)
+    out_s = ntc.decode(model, q, leaky_slope=slope, out_dtype=dtype)
+    ref = oracle.decode(w, leaky_slope=slope or 0.0)
+    err = np.abs(out_b.cpu().numpy().astype(np.float64) - ref).max()
+    say(f"    max abs err {err:.3e}")
+    assert err <= TOL
+    iv = torch.int16 if dtype == torch.float16 else torch.int32
+    assert torch.equal(out_b.view(iv), out_s.view(iv))

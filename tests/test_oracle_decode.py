@@ -227,3 +227,96 @@ def test_leaky_slope_zero_is_relu(oracle):
     w = make_workload([16, 8], [8, 8], T=4, dims=[16, 32, 32, 3], D=2, n=300, seed=21)
     assert np.array_equal(oracle.decode(w, leaky_slope=0.0), oracle.decode(w))
     assert not np.array_equal(oracle.decode(w, leaky_slope=0.1), oracle.decode(w))
+
+
+# ------------------------------------------------------------ positional encoding
+# The Sec. 4 setup concatenates a positional encoding to the encoder output; its
+# form is a reading (octave k: sin, cos of 2^k pi u, then of 2^k pi v).  The pins
+# below fix the order of the four values, the octave scaling and the placement
+# after the latent features, and relate the decoder with encoding to the pinned
+# decoder without it.
+
+def pe_columns(oracle, w, K):
+    F = int(sum(w.channels))
+    f = oracle.features(w, pe_octaves=K)
+    assert f.shape[1] == F + 4 * K
+    np.testing.assert_array_equal(f[:, :F], oracle.features(w, pe_octaves=0))
+    return f[:, F:]
+
+
+def test_pe_special_points(oracle):
+    """u = 1/2, v = 0 and u = 1/4, v = 3/4: values fixed by the unit circle."""
+    uv = np.array([[0.5, 0.0], [0.25, 0.75]], np.float32)
+    w = make_workload([16], [8], T=1, dims=[8, 8], D=1, n=2, seed=30, uv=uv,
+                      tex=np.zeros(2, np.uint32))
+    pe = pe_columns(oracle, w, 4)
+    r2 = np.sqrt(0.5)
+    # octave k of (u, v): sin(2^k pi u), cos(2^k pi u), sin(2^k pi v), cos(2^k pi v)
+    want0 = [1, 0, 0, 1,  0, -1, 0, 1,  0, 1, 0, 1,  0, 1, 0, 1]
+    want1 = [r2, r2, r2, -r2,  1, 0, -1, 0,  0, -1, 0, -1,  0, 1, 0, 1]
+    np.testing.assert_allclose(pe[0], want0, atol=1e-15)
+    np.testing.assert_allclose(pe[1], want1, atol=1e-15)
+    # u = v = 0: every sine exactly 0, every cosine exactly 1
+    w0 = make_workload([16], [8], T=1, dims=[8, 8], D=1, n=1, seed=31,
+                       uv=np.zeros((1, 2), np.float32), tex=np.zeros(1, np.uint32))
+    assert np.array_equal(pe_columns(oracle, w0, 8)[0], np.tile([0.0, 1.0, 0.0, 1.0], 8))
+
+
+def test_pe_octaves_double_the_angle(oracle):
+    """sin(2a) = 2 sin(a) cos(a), cos(2a) = cos^2(a) - sin^2(a) between octaves
+    k and k+1, and sin^2 + cos^2 = 1, for random coordinates inside and outside
+    [0, 1)."""
+    w = make_workload([16], [8], T=2, dims=[8, 8], D=1, n=300, seed=32)
+    pe = pe_columns(oracle, w, 8).reshape(-1, 8, 4)
+    for c in (0, 2):  # u, v
+        s, co = pe[:, :, c], pe[:, :, c + 1]
+        np.testing.assert_allclose(s ** 2 + co ** 2, 1.0, atol=1e-14)
+        np.testing.assert_allclose(s[:, 1:], 2 * s[:, :-1] * co[:, :-1], atol=1e-12)
+        np.testing.assert_allclose(co[:, 1:], co[:, :-1] ** 2 - s[:, :-1] ** 2, atol=1e-12)
+    # octave 0 against the coordinate itself
+    np.testing.assert_allclose(pe[:, 0, 0], np.sin(np.pi * w.uv[:, 0].astype(np.float64)),
+                               atol=1e-15)
+
+
+def test_pe_zero_columns_equal_decoder_without_pe(oracle):
+    """A decoder whose weights on the encoding are zero gives the output of the
+    same decoder restricted to the latent features (the pinned path)."""
+    base = make_workload([16, 8], [8, 8], T=4, dims=[16, 32, 32, 3], D=2, n=300, seed=33)
+    K = 4
+    rng = np.random.default_rng(34)
+    blob_pe, blob = [], []
+    for _ in range(2):
+        w0 = rng.uniform(-0.5, 0.5, (32, 16))
+        w0pe = np.concatenate([w0, np.zeros((32, 4 * K))], axis=1)
+        rest = [rng.uniform(-0.1, 0.1, 32), rng.uniform(-0.3, 0.3, (32, 32)),
+                rng.uniform(-0.1, 0.1, 32), rng.uniform(-0.3, 0.3, (3, 32)), rng.uniform(-0.1, 0.1, 3)]
+        blob_pe += [w0pe.ravel()] + [r.ravel() for r in rest]
+        blob += [w0.ravel()] + [r.ravel() for r in rest]
+    w_no = W.Workload("t", base.n_textures, base.res, base.channels, base.latents, 2, [16, 32, 32, 3],
+                      W.fp16_bits(np.concatenate(blob)), base.tex_to_dec, base.tex_id, base.uv, None)
+    w_pe = W.Workload("t", base.n_textures, base.res, base.channels, base.latents, 2,
+                      [16 + 4 * K, 32, 32, 3], W.fp16_bits(np.concatenate(blob_pe)),
+                      base.tex_to_dec, base.tex_id, base.uv, None, pe_octaves=K)
+    assert np.array_equal(oracle.decode(w_pe), oracle.decode(w_no))
+
+
+def test_pe_only_decoder_ignores_latents(oracle):
+    """With zero weights on the latent features the output depends on (u, v)
+    only: redrawing the latents leaves it unchanged, moving u changes it."""
+    K = 4
+    w = make_workload([16, 8], [8, 8], T=4, dims=[16 + 4 * K, 32, 32, 8], D=2, n=300, seed=35)
+    w.pe_octaves = K
+    p = W.bits_to_f32(w.params).astype(np.float64).copy()
+    stride = W.decoder_stride(w.dims)
+    for d in range(2):
+        W0 = p[d * stride: d * stride + 32 * (16 + 4 * K)].reshape(32, 16 + 4 * K)
+        W0[:, :16] = 0.0
+    w.params = W.fp16_bits(p)
+    y = oracle.decode(w)
+    w2 = make_workload([16, 8], [8, 8], T=4, dims=w.dims, D=2, n=300, seed=36, params=w.params,
+                       tex=w.tex_id, t2d=w.tex_to_dec, uv=w.uv)
+    w2.pe_octaves = K
+    assert not np.array_equal(w2.latents, w.latents)
+    assert np.array_equal(oracle.decode(w2), y)
+    w2.uv = (w.uv + np.float32(0.125)).astype(np.float32)
+    assert not np.allclose(oracle.decode(w2), y)
