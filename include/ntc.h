@@ -193,10 +193,29 @@ typedef struct {
   float leaky_slope;         /* NTC_ACT_LEAKY_RELU only: 0 < slope < 1 (held as fp16) */
   int32_t output_format;     /* NTC_OUT_F32 or NTC_OUT_F16 */
   int32_t pe_octaves;        /* positional-encoding octaves K: 0, 4 or 8 */
+  int32_t engine;            /* NTC_ENGINE_MFMA or NTC_ENGINE_FMA */
 } ntc_decode_options;
 
 /*
- * ntc_decode with options (NULL = ReLU and float rows, i.e. ntc_decode).  `out`
+ * Engines (Sec. 4.4 compares a shared decoder with two non-shared
+ * implementations, one on tensor instructions and one on plain fused
+ * multiply-adds):
+ *   NTC_ENGINE_MFMA: the MLP runs on MFMA once per decoder present in a wave
+ *     (ntc_decode's engine); binned or stream mode.
+ *   NTC_ENGINE_FMA: every lane evaluates its own query's decoder with vector
+ *     fp16 dot products (fp32 accumulation), reading that decoder's weights
+ *     itself, so a wave's cost does not depend on how many decoders it holds
+ *     (the paper's Non-Shared FMA).  Stream mode only (NTC_ERR_UNSUPPORTED with
+ *     bin_offset); dims[n_layers] must be 8 or 16 (NTC_ERR_UNSUPPORTED) and
+ *     decoders->params 16-byte aligned (NTC_ERR_ARG).  Results agree with the
+ *     MFMA engine within rounding, not bit for bit.
+ */
+#define NTC_ENGINE_MFMA 0
+#define NTC_ENGINE_FMA 1
+
+/*
+ * ntc_decode with options (NULL = ReLU, float rows and the MFMA engine, i.e.
+ * ntc_decode).  `out`
  * holds n * dims[n_layers] elements of the chosen format, rows in original
  * query order; with NTC_OUT_F16 the bytes are n * dims[n_layers] * 2 (same
  * 4 GiB - 512 limit).  LeakyReLU is applied to the fp16-rounded pre-activation,

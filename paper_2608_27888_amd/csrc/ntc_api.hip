@@ -73,7 +73,7 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
                   int64_t perm_capacity, int32_t align, const ntc_decode_options *opt,
                   void *out, void *stream) {
   if (!g || !m || !q) return NTC_ERR_ARG;
-  ntc_decode_options o = {NTC_ACT_RELU, 0.f, NTC_OUT_F32, 0};
+  ntc_decode_options o = {NTC_ACT_RELU, 0.f, NTC_OUT_F32, 0, NTC_ENGINE_MFMA};
   if (opt) o = *opt;
   if (o.hidden_activation != NTC_ACT_RELU && o.hidden_activation != NTC_ACT_LEAKY_RELU)
     return NTC_ERR_ARG;
@@ -81,6 +81,8 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
     return NTC_ERR_ARG;
   if (o.output_format != NTC_OUT_F32 && o.output_format != NTC_OUT_F16) return NTC_ERR_ARG;
   if (o.pe_octaves != 0 && o.pe_octaves != 4 && o.pe_octaves != 8) return NTC_ERR_ARG;
+  if (o.engine != NTC_ENGINE_MFMA && o.engine != NTC_ENGINE_FMA) return NTC_ERR_ARG;
+  const bool fma = o.engine == NTC_ENGINE_FMA;
   const int64_t elem = o.output_format == NTC_OUT_F16 ? 2 : 4;
   if (q->n < 0 || q->n > kMaxQueries) return NTC_ERR_ARG;
   if (g->n_textures < 1 || g->n_levels < 1 || g->n_levels > NTC_MAX_LEVELS) return NTC_ERR_ARG;
@@ -90,6 +92,8 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
   const bool binned = bin_offset != nullptr;
   if (q->n > 0 && (!g->latents || !m->params || !q->tex_id || !q->uv || !out))
     return NTC_ERR_ARG;
+  // the FMA engine reads 16-byte weight vectors straight from the parameter block
+  if (fma && ((uintptr_t)m->params & 15)) return NTC_ERR_ARG;
   if (binned) {
     if (!perm || align < 64 || !pow2(align) || align > NTC_MAX_ALIGN) return NTC_ERR_ARG;
     if (perm_capacity < ntc_bins_capacity(q->n, m->n_decoders, align)) return NTC_ERR_CAPACITY;
@@ -153,6 +157,12 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
   a.slope_h2 = (uint32_t)__builtin_bit_cast(uint16_t, slope) * 0x00010001u;
   a.out_f16 = o.output_format == NTC_OUT_F16;
   a.pe_octaves = o.pe_octaves;
+  if (fma) {
+    if (binned) return NTC_ERR_UNSUPPORTED;  // per-lane decoders: stream order only
+    if (out_dim % 8 != 0) return NTC_ERR_UNSUPPORTED;
+    if (q->n == 0) return NTC_OK;
+    return launch_decode_fma(a, L, ch, hid, (hipStream_t)stream);
+  }
   if (q->n == 0) return NTC_OK;
   return launch_decode(a, L, ch, F, hid, (hipStream_t)stream);
 }

@@ -30,6 +30,9 @@
 // features once, then loops over the distinct decoders present; every wave
 // that holds queries of that decoder runs its full MLP and keeps the results
 // of those lanes only.
+//
+// A second engine (decode_fma, end of the file) evaluates the MLP per lane with
+// vector dot products instead: the paper's Non-Shared FMA comparison.
 #include "ntc_internal.h"
 
 namespace ntc {
@@ -962,7 +965,166 @@ int launch_hidden(const DecodeArgs &a, hipStream_t stream) {
   }
 }
 
+// ------------------------------------------------- non-shared FMA decode
+//
+// The paper's Non-Shared FMA comparison (Sec. 4.4): every lane evaluates the
+// decoder of its own query with vector instructions, so lanes that use
+// different decoders share one instruction stream and differ only in the
+// addresses their weights come from; the cost does not grow with the number of
+// decoders in a wave, unlike the tensor path's one pass per decoder.  Products
+// are v_dot2c_f32_f16 (two fp16 products added to an fp32 accumulator), with
+// the tensor path's fp16 features and fp16-rounded activations, so both engines
+// compute the same function within rounding.
+//
+// One thread per query, stream order.  Row j of W_i is read by the lane as
+// din / 8 16-byte loads from the lane's decoder block (L1/L2-cached).  A layer
+// takes its input from registers and writes its output, as fp16 pairs, to the
+// thread's own LDS column (word i at i * kBlock + thread): the row loop is a
+// runtime loop, and registers cannot be indexed at run time.
+
+__device__ __forceinline__ float dot2(uint32_t w, uint32_t h, float c) {
+  return __builtin_amdgcn_fdot2(as_h2(w), as_h2(h), c, false);
+}
+
+// fp16 pair of two fp32 values.
+__device__ __forceinline__ float2 unpack_half2(uint32_t v) {
+  const half2v h = as_h2(v);
+  return float2{(float)h[0], (float)h[1]};
+}
+
+// Layer din -> dout (dout even) with its input h (fp16 pairs) in registers.
+// Hidden layers (OUT = false) write the activated outputs as fp16 pairs, word
+// j / 2 of the thread's LDS column; the output layer (OUT = true) writes the
+// sigmoid of each output as a float, word j.
+template <int DIN, bool OUT>
+__device__ __forceinline__ void fma_layer(const uint16_t *W, int dout, const uint32_t (&h)[DIN / 2],
+                                          uint32_t *col, bool leaky, uint32_t slope_h2) {
+  const uint16_t *b = W + (size_t)dout * DIN;
+#pragma unroll 2
+  for (int j = 0; j < dout; j += 2) {
+    const float2 bj = unpack_half2(*(const uint32_t *)(b + j));
+    float acc0 = bj.x, acc1 = bj.y;
+    const u32x4 *r0 = (const u32x4 *)(W + (size_t)j * DIN);
+    const u32x4 *r1 = (const u32x4 *)(W + (size_t)(j + 1) * DIN);
+#pragma unroll
+    for (int k = 0; k < DIN / 8; ++k) {
+      const u32x4 w0 = r0[k], w1 = r1[k];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc0 = dot2(w0[e], h[4 * k + e], acc0);
+        acc1 = dot2(w1[e], h[4 * k + e], acc1);
+      }
+    }
+    if constexpr (OUT) {
+      col[j * kBlock] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(acc0 * -kLog2e)));
+      col[(j + 1) * kBlock] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(acc1 * -kLog2e)));
+    } else {
+      col[(j / 2) * kBlock] = leaky ? leaky_pack2(acc0, acc1, slope_h2) : relu_pack2(acc0, acc1);
+    }
+  }
+}
+
+// Words of a thread's LDS column: the widest hidden layer as fp16 pairs, or the
+// output row as floats.
+template <int HID>
+constexpr int kFmaColumn = HID / 2 > 16 ? HID / 2 : 16;
+
+template <int NL, int CH, int PE, int HID, bool MIP>
+__global__ void __launch_bounds__(kBlock, 2) decode_fma(const DecodeArgs a) {
+  using S = Shape<NL, CH, PE, HID>;
+  extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
+  uint32_t *col = lds + threadIdx.x;  // this thread's activations, stride kBlock
+  const uint64_t q64 = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (q64 >= a.n) return;
+  const uint32_t q = (uint32_t)q64;
+  const Query qq = validate(a, load_query<NL, MIP>(a, q, true));
+  if (!qq.valid) return;
+  const uint32_t d = a.tex_to_dec[qq.tex];
+  if (d >= (uint32_t)a.n_decoders) return;
+  const uint16_t *p = a.params + (size_t)d * (size_t)a.dec_stride;
+  const bool leaky = a.leaky != 0;
+  {  // layer 0: F -> HID
+    uint32_t x[S::F / 2];
+    gather<NL, CH, PE, MIP>(a, qq, x);
+    fma_layer<S::F, false>(p, HID, x, col, leaky, a.slope_h2);
+    p += (size_t)HID * (S::F + 1);
+  }
+  // hidden -> hidden, then the output layer (8 or 16 wide, sigmoid)
+  for (int l = 0; l <= a.n_hidden; ++l) {
+    uint32_t h[HID / 2];
+#pragma unroll
+    for (int i = 0; i < HID / 2; ++i) h[i] = col[i * kBlock];
+    if (l < a.n_hidden) {
+      fma_layer<HID, false>(p, HID, h, col, leaky, a.slope_h2);
+      p += (size_t)HID * (HID + 1);
+    } else {
+      fma_layer<HID, true>(p, a.out_dim, h, col, leaky, a.slope_h2);
+    }
+  }
+  const int out_dim = a.out_dim;
+  float y[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) y[c] = c < out_dim ? __builtin_bit_cast(float, col[c * kBlock]) : 0.f;
+  if (a.out_f16) {
+    u32x2 *o = (u32x2 *)((uint16_t *)a.out + (size_t)q * out_dim);
+#pragma unroll
+    for (int c = 0; c < 16; c += 4)
+      if (c < out_dim) o[c / 4] = u32x2{pack_half2(y[c], y[c + 1]), pack_half2(y[c + 2], y[c + 3])};
+  } else {
+    floatx4 *o = (floatx4 *)((float *)a.out + (size_t)q * out_dim);
+#pragma unroll
+    for (int c = 0; c < 16; c += 4)
+      if (c < out_dim) o[c / 4] = floatx4{y[c], y[c + 1], y[c + 2], y[c + 3]};
+  }
+}
+
+template <int NL, int CH, int PE, int HID, bool MIP>
+int launch_fma(const DecodeArgs &a, hipStream_t stream) {
+  const void *fn = (const void *)decode_fma<NL, CH, PE, HID, MIP>;
+  const size_t lds = (size_t)kFmaColumn<HID> * kBlock * sizeof(uint32_t);
+  if (lds > 64 * 1024 &&
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return NTC_ERR_HIP;
+  const uint64_t blocks = ((uint64_t)a.n + kBlock - 1) / kBlock;
+  hipLaunchKernelGGL((decode_fma<NL, CH, PE, HID, MIP>), dim3((unsigned)blocks), dim3(kBlock), lds,
+                     stream, a);
+  return hip_status(hipGetLastError());
+}
+
+template <int NL, int CH, int PE, int HID>
+int launch_fma_mip(const DecodeArgs &a, hipStream_t stream) {
+  if constexpr (PE > 0) {
+    return a.mip ? NTC_ERR_UNSUPPORTED : launch_fma<NL, CH, PE, HID, false>(a, stream);
+  } else {
+    return a.mip ? launch_fma<NL, CH, PE, HID, true>(a, stream)
+                 : launch_fma<NL, CH, PE, HID, false>(a, stream);
+  }
+}
+
 }  // namespace
+
+int launch_decode_fma(const DecodeArgs &a, int n_levels, int channels, int hidden,
+                      hipStream_t stream) {
+  if (a.out_dim % 8 != 0) return NTC_ERR_UNSUPPORTED;
+  if (a.n_hidden < 1 || a.n_hidden > 2) return NTC_ERR_UNSUPPORTED;
+  if (a.pe_octaves == 0) {
+    if (hidden == 64) {
+      if (n_levels == 2 && channels == 8) return launch_fma_mip<2, 8, 0, 64>(a, stream);
+      if (n_levels == 2 && channels == 16) return launch_fma_mip<2, 16, 0, 64>(a, stream);
+      if (n_levels == 3 && channels == 16) return launch_fma_mip<3, 16, 0, 64>(a, stream);
+    } else if (hidden == 128) {
+      if (n_levels == 2 && channels == 8) return launch_fma_mip<2, 8, 0, 128>(a, stream);
+      if (n_levels == 2 && channels == 16) return launch_fma_mip<2, 16, 0, 128>(a, stream);
+      if (n_levels == 3 && channels == 16) return launch_fma_mip<3, 16, 0, 128>(a, stream);
+    }
+  } else if (hidden == 64 && n_levels == 2 && a.n_hidden == 1) {
+    if (channels == 8 && a.pe_octaves == 4) return launch_fma_mip<2, 8, 16, 64>(a, stream);
+    if (channels == 8 && a.pe_octaves == 8) return launch_fma_mip<2, 8, 32, 64>(a, stream);
+    if (channels == 16 && a.pe_octaves == 4) return launch_fma_mip<2, 16, 16, 64>(a, stream);
+    if (channels == 16 && a.pe_octaves == 8) return launch_fma_mip<2, 16, 32, 64>(a, stream);
+  }
+  return NTC_ERR_UNSUPPORTED;
+}
 
 int launch_decode(const DecodeArgs &a, int n_levels, int channels, int feat, int hidden,
                   hipStream_t stream) {

@@ -102,6 +102,9 @@ struct DecodeArgs {
 // Returns NTC_ERR_UNSUPPORTED when no kernel is built for the shape.
 int launch_decode(const DecodeArgs &a, int n_levels, int channels, int feat, int hidden,
                   hipStream_t stream);
+// Per-lane vector-FMA decode in stream order (NTC_ENGINE_FMA); same contract.
+int launch_decode_fma(const DecodeArgs &a, int n_levels, int channels, int hidden,
+                      hipStream_t stream);
 
 inline int hip_status(hipError_t e) { return e == hipSuccess ? NTC_OK : NTC_ERR_HIP; }
 

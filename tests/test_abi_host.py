@@ -191,3 +191,46 @@ def test_decode_options_validation(L):
     for i, v in enumerate((48, 64, 64, 64, 8)):
         d.dims[i] = v
     assert call(ntc.NTC_ACT_RELU, 0.0, 0, pe=4) == ntc.NTC_ERR_UNSUPPORTED  # two hidden->hidden
+
+
+def test_decode_engine_validation(L):
+    """The FMA engine (the paper's Non-Shared FMA, Sec. 4.4): stream mode only,
+    8- or 16-wide outputs, 16-byte aligned parameters; an unknown engine is an
+    argument error."""
+    g = ntc.Grids()
+    g.n_textures, g.n_levels = 4, 2
+    for i, (r, c) in enumerate(zip((256, 128), (16, 16))):
+        g.res[i], g.channels[i] = r, c
+    g.latents = FAKE
+    d = ntc.Decoders()
+    d.n_decoders, d.n_layers = 4, 3
+    for i, v in enumerate((32, 64, 64, 8)):
+        d.dims[i] = v
+    d.params = FAKE
+    q = ntc.Queries()
+    q.tex_id, q.uv, q.mip, q.n = FAKE, FAKE, None, 100
+
+    def call(engine, binned=False, n=100):
+        q.n = n
+        o = ntc.DecodeOptions(ntc.NTC_ACT_RELU, 0.0, ntc.NTC_OUT_F32, 0, engine)
+        cap = ntc.perm_capacity(n, 4, 64)
+        return L.ntc_decode_ex(ctypes.byref(g), ctypes.byref(d), FAKE, ctypes.byref(q),
+                               FAKE if binned else None, FAKE if binned else None, cap,
+                               64 if binned else 0, ctypes.byref(o), FAKE, None)
+
+    assert call(2) == ntc.NTC_ERR_ARG
+    assert call(-1) == ntc.NTC_ERR_ARG
+    assert call(ntc.NTC_ENGINE_FMA, binned=True) == ntc.NTC_ERR_UNSUPPORTED
+    assert call(ntc.NTC_ENGINE_FMA, n=0) == ntc.NTC_OK
+    if not HAS_DEVICE:
+        assert call(ntc.NTC_ENGINE_FMA) == ntc.NTC_ERR_HIP  # built: launches on FAKE
+    d.params = ctypes.c_void_p(0x100000 + 8)
+    assert call(ntc.NTC_ENGINE_FMA) == ntc.NTC_ERR_ARG     # not 16-byte aligned
+    assert call(ntc.NTC_ENGINE_MFMA, n=0) == ntc.NTC_OK    # the MFMA engine has no such need
+    d.params = FAKE
+    for out_dim in (3, 4, 12):
+        d.dims[3] = out_dim
+        assert call(ntc.NTC_ENGINE_FMA) == ntc.NTC_ERR_UNSUPPORTED
+    d.dims[3] = 16
+    if not HAS_DEVICE:
+        assert call(ntc.NTC_ENGINE_FMA) == ntc.NTC_ERR_HIP

@@ -315,3 +315,70 @@ def test_decode_positional_encoding(dev, oracle, name, octaves, dims, slope, dty
     assert err <= TOL
     iv = torch.int16 if dtype == torch.float16 else torch.int32
     assert torch.equal(out_b.view(iv), out_s.view(iv))
+
+
+FMA_CASES = [  # (config, MLP widths or None, LeakyReLU slope or None, output dtype, PE octaves)
+    ("tiny", None, None, torch.float32, 0),
+    ("single", None, None, torch.float32, 0),
+    ("divergent", None, None, torch.float32, 0),
+    ("clustered4k_d512", None, 0.01, torch.float16, 0),
+    ("k10_per_wave", None, None, torch.float32, 0),
+    ("wide_trilinear", None, None, torch.float32, 0),           # mip blending, 128 wide
+    ("wide_trilinear_d512", None, 0.05, torch.float16, 0),
+    ("single", [32, 64, 64, 64, 16], None, torch.float32, 0),   # two hidden->hidden layers
+    ("tiny", [16, 128, 128, 8], None, torch.float16, 0),
+    ("clustered4k", None, 0.01, torch.float32, 4),              # positional encoding
+    ("tiny", [48, 64, 64, 8], 0.01, torch.float16, 8),
+]
+
+
+@pytest.mark.parametrize("name,dims,slope,dtype,pe", FMA_CASES)
+def test_decode_fma_engine(dev, oracle, name, dims, slope, dtype, pe):
+    """The per-lane vector-FMA engine (the paper's Non-Shared FMA, Sec. 4.4)
+    against the oracle, in stream order with every decoder mix of the small
+    configurations; it computes the same function as the MFMA engine within
+    rounding."""
+    w = small(name)
+    if pe:
+        w = w.with_pe(pe, dims, seed=7)
+    elif dims is not None:
+        w = w.with_dims(dims, seed=3)
+    say(f"[fma] {name} dims={w.dims} slope={slope} {dtype} pe={pe} n={w.n} D={w.n_decoders}")
+    model, q = ntc.upload(w, dev)
+    out_f = ntc.decode(model, q, leaky_slope=slope, out_dtype=dtype, engine="fma")
+    out_m = ntc.decode(model, q, leaky_slope=slope, out_dtype=dtype)
+    ref = oracle.decode(w, leaky_slope=slope or 0.0)
+    yf = out_f.cpu().numpy().astype(np.float64)
+    err = np.abs(yf - ref).max()
+    say(f"    max abs err {err:.3e} (vs MFMA engine {np.abs(yf - out_m.cpu().numpy()).max():.2e})")
+    assert err <= TOL
+    assert np.all((yf >= 0) & (yf <= 1))
+
+
+def test_decode_fma_invalid_queries_untouched(dev, oracle):
+    w = W.small("tiny")
+    w.tex_id = w.tex_id.copy()
+    w.tex_id[::13] = 7
+    w.tex_to_dec = np.array([0, 1, 0, 9], np.uint32)
+    say("[fma-invalid] tiny with bad ids")
+    model, q = ntc.upload(w, dev)
+    out = torch.full((w.n, w.out_dim), -12345.0, device=dev)
+    ntc.decode(model, q, out=out, engine="fma")
+    ref = oracle.decode(w)
+    bad = np.isnan(ref[:, 0])
+    o = out.cpu().numpy()
+    assert bad.sum() > 0 and np.all(o[bad] == -12345.0)
+    assert np.abs(o[~bad] - ref[~bad]).max() <= TOL
+
+
+@pytest.mark.parametrize("n", [1, 63, 65, 255, 257, 4097])
+def test_decode_fma_ragged_sizes(dev, oracle, n):
+    w = W.small("clustered4k")
+    w.tex_id, w.uv = w.tex_id[:n].copy(), w.uv[:n].copy()
+    say(f"[fma-ragged] n={n}")
+    model, q = ntc.upload(w, dev)
+    out = torch.full((n + 7, w.out_dim), -3.0, device=dev)
+    ntc.decode(model, q, out=out[:n], engine="fma")
+    o = out.cpu().numpy()
+    assert np.abs(o[:n] - oracle.decode(w)).max() <= TOL
+    assert np.all(o[n:] == -3.0)  # nothing written past the last row
