@@ -23,13 +23,14 @@
 // and the permutation is unique.  A row whose queries all share the decoder of
 // the previous such row (the common case for screen-coherent material maps)
 // touches no LDS: the wave keeps that decoder's count or cursor in a register.
-// Each lane issues a whole batch of loads before it consumes any of them.
+// Each lane issues a whole batch of loads (and the batch's map lookups) before
+// it consumes any of them, and fetches the next batch while it counts this one.
 #include "ntc_internal.h"
 
 namespace ntc {
 namespace {
 
-constexpr int kRowsPerBatch = 16;                                 // rows a wave loads at once
+constexpr int kRowsPerBatch = 8;                                  // rows a wave loads at once
 constexpr int64_t kWaveQuantum = (int64_t)kWave * kRowsPerBatch;  // queries per wave batch
 constexpr int64_t kChunkQuantum = kWaveQuantum * kWavesPerBlock;  // chunks are multiples of this
 constexpr int64_t kMinChunk = 2 * kChunkQuantum;                  // queries per workgroup, at least
@@ -71,25 +72,47 @@ bins_hist(const uint32_t *__restrict__ tex_id, uint32_t n,
   extern __shared__ uint32_t lds[];  // kWavesPerBlock x (n_decoders + 1) counters
   const uint32_t b = blockIdx.x, w = threadIdx.x / kWave, lane = lane_id();
   const uint32_t rows = n_decoders + 1;
-  for (uint32_t i = threadIdx.x; i < kWavesPerBlock * rows; i += kBlock) lds[i] = 0;
-  __syncthreads();
-  uint32_t *h = lds + w * rows;
   const Slice sl = slice_of(b, w, chunk, n);
   // A run of whole rows with one decoder is counted in (run_d, run_n) and
   // added to the histogram when it ends.
   uint32_t run_d = kOutside, run_n = 0;
-  for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
-    uint32_t t[kRowsPerBatch];
+  // Lanes past the slice load its first id (an unconditional load keeps the
+  // compiler's wait counts exact); the row loop masks them out.
+  auto fetch = [&](uint64_t base, uint32_t (&v)[kRowsPerBatch]) {
 #pragma unroll
     for (int j = 0; j < kRowsPerBatch; ++j) {
       const uint64_t q = base + (uint64_t)j * kWave + lane;
-      t[j] = q < sl.end ? tex_id[q] : kOutside;
+      v[j] = tex_id[q < sl.end ? q : sl.beg];
     }
+  };
+  // the first batch is in flight while the histogram is cleared
+  uint32_t nxt[kRowsPerBatch];
+  if (sl.beg < sl.end) fetch(sl.beg, nxt);
+  for (uint32_t i = threadIdx.x; i < kWavesPerBlock * rows; i += kBlock) lds[i] = 0;
+  __syncthreads();
+  uint32_t *h = lds + w * rows;
+  for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
+    uint32_t t[kRowsPerBatch];
+#pragma unroll
+    for (int j = 0; j < kRowsPerBatch; ++j) t[j] = nxt[j];
+    // Every row's map lookup is issued before any of them is used: the loads
+    // are unconditional (texture 0 stands in for an out-of-range id or a lane
+    // past the slice), so they are not serialised behind per-row branches.
+    // They go out before the next batch's ids, so that waiting for them does
+    // not wait for that prefetch (loads complete in issue order for the
+    // wait counter).
+    uint32_t m[kRowsPerBatch];
+#pragma unroll
+    for (int j = 0; j < kRowsPerBatch; ++j) m[j] = tex_to_dec[t[j] < n_textures ? t[j] : 0u];
+    __builtin_amdgcn_sched_barrier(0);
+    if (base + kWaveQuantum < sl.end) fetch(base + kWaveQuantum, nxt);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < kRowsPerBatch; ++j) {
       const uint64_t q = base + (uint64_t)j * kWave + lane;
       const bool inside = q < sl.end;
-      const uint32_t d = inside ? decoder_of(t[j], tex_to_dec, n_textures, n_decoders) : kOutside;
+      const uint32_t d = !inside ? kOutside
+                         : (t[j] < n_textures && m[j] < n_decoders) ? m[j] : n_decoders;
       if (inside) dec16[q] = d < n_decoders ? (uint16_t)d : kInvalid16;
       const uint32_t v0 = __builtin_amdgcn_readfirstlane(d);
       if (ballot(d == v0) == ~0ull) {
@@ -181,6 +204,18 @@ bins_scatter(const uint16_t *__restrict__ dec16, uint32_t n, uint32_t n_decoders
   __shared__ uint32_t lds_tmp[kWavesPerBlock];
   const uint32_t b = blockIdx.x, w = threadIdx.x / kWave, lane = lane_id();
   const uint32_t nblocks = gridDim.x;
+  const Slice sl = slice_of(b, w, chunk, n);
+  // Lanes past the slice read as invalid.  The first batch is in flight
+  // during the offset scan below.
+  auto fetch = [&](uint64_t base, uint32_t (&v)[kRowsPerBatch]) {
+#pragma unroll
+    for (int j = 0; j < kRowsPerBatch; ++j) {
+      const uint64_t q = base + (uint64_t)j * kWave + lane;
+      v[j] = q < sl.end ? dec16[q] : kInvalid16;
+    }
+  };
+  uint32_t nxt[kRowsPerBatch];
+  if (sl.beg < sl.end) fetch(sl.beg, nxt);
   // Padded bin offsets: thread i owns decoders [dlo, dhi).
   const uint32_t dper = (n_decoders + kBlock - 1) / kBlock;
   const uint32_t dlo = min(threadIdx.x * dper, n_decoders);
@@ -203,19 +238,9 @@ bins_scatter(const uint16_t *__restrict__ dec16, uint32_t n, uint32_t n_decoders
   if (b == 0 && threadIdx.x == 0) bin_offset[n_decoders] = total;
   __syncthreads();
   uint32_t *cur = lds + w * n_decoders;
-  const Slice sl = slice_of(b, w, chunk, n);
-  auto fetch = [&](uint64_t base, uint32_t (&v)[kRowsPerBatch]) {
-#pragma unroll
-    for (int j = 0; j < kRowsPerBatch; ++j) {
-      const uint64_t q = base + (uint64_t)j * kWave + lane;
-      v[j] = q < sl.end ? dec16[q] : kInvalid16;
-    }
-  };
   // (cd, cc): a decoder whose cursor lives in a register while whole rows of
   // it follow one another; cur[cd] is stale meanwhile.
   uint32_t cd = kOutside, cc = 0;
-  uint32_t nxt[kRowsPerBatch];
-  if (sl.beg < sl.end) fetch(sl.beg, nxt);
   for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
     uint32_t v[kRowsPerBatch];
 #pragma unroll
