@@ -100,56 +100,90 @@ __host__ __device__ inline Image image_of(int n_hidden) {
   return im;
 }
 
+// Source of lane-slice lf of the image: the layer's weight block and the row,
+// K-slice, half and shape that select its 8 weights.
+template <int NL, int CH, int PE, int HID>
+struct SliceSource {
+  size_t woff;  // offset of W_layer inside the decoder's parameter block
+  int layer, row, s, h, din, dout;
+};
+
+template <int NL, int CH, int PE, int HID>
+__device__ __forceinline__ SliceSource<NL, CH, PE, HID> slice_source(const DecodeArgs &a, int lf) {
+  using S = Shape<NL, CH, PE, HID>;
+  SliceSource<NL, CH, PE, HID> r;
+  const int f = lf / kWave, lane = lf % kWave;
+  int mb;
+  if (f < S::MB * S::KS0) {
+    r.layer = 0; mb = f / S::KS0; r.s = f % S::KS0; r.din = S::F; r.dout = HID;
+  } else if (f < S::MB * S::KS0 + a.n_hidden * S::MB * S::KSH) {
+    const int g = f - S::MB * S::KS0;
+    r.layer = 1 + g / (S::MB * S::KSH);
+    const int q = g % (S::MB * S::KSH);
+    mb = q / S::KSH; r.s = q % S::KSH; r.din = HID; r.dout = HID;
+  } else {
+    r.layer = a.n_hidden + 1; mb = 0; r.s = f - S::MB * S::KS0 - a.n_hidden * S::MB * S::KSH;
+    r.din = HID; r.dout = a.out_dim;
+  }
+  r.woff = r.layer == 0 ? 0 : (size_t)HID * (S::F + 1) + (size_t)(r.layer - 1) * HID * (HID + 1);
+  r.row = mb * 32 + (lane & 31);
+  r.h = lane >> 5;
+  return r;
+}
+
+// Weight unit that element e of a lane-slice holds (layer 0 reads the
+// features in order; later layers read the previous layer's accumulator
+// order, see sigma16).
+template <int NL, int CH, int PE, int HID>
+__device__ __forceinline__ int slice_unit(const SliceSource<NL, CH, PE, HID> &r, int e) {
+  const int kap = 8 * r.h + e;
+  return 16 * r.s + (r.layer == 0 ? kap : sigma16(kap));
+}
+
 // Copies decoder `dec` into the LDS image, re-arranged into A fragments; all
 // threads of the workgroup take part; the caller brackets it with barriers.
+// The decoder block is read through a raw buffer resource: 32-bit offsets, and
+// a weight outside its layer (padding rows and columns) gets an offset past
+// the block, which the hardware returns as zero.  A thread issues the loads of
+// kStageSlices lane-slices (8 weights each) back to back, so staging costs one
+// memory round trip per kStageSlices * THREADS lane-slices.
+constexpr int kStageSlices = 2;
+constexpr uint32_t kPastBlock = 0xFFFFFF00u;  // byte offset past any decoder block
+
 template <int NL, int CH, int PE, int HID, int THREADS>
 __device__ void stage_decoder(const DecodeArgs &a, uint32_t dec, uint32_t *lds) {
-  using S = Shape<NL, CH, PE, HID>;
   const Image im = image_of<NL, CH, PE, HID>(a.n_hidden);
   const uint16_t *p = a.params + (size_t)dec * (size_t)a.dec_stride;
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void *)p, 0, (int)(a.dec_stride * 2), 0x00020000);
   const int n_layers = a.n_hidden + 2;
-  // fragment lane-slices: one 16-byte lane slice per iteration
-  for (int lf = threadIdx.x; lf < im.n_frags * kWave; lf += THREADS) {
-    const int f = lf / kWave, lane = lf % kWave;
-    int layer, mb, s, ks, din, dout;
-    if (f < S::MB * S::KS0) {
-      layer = 0; mb = f / S::KS0; s = f % S::KS0; ks = S::KS0; din = S::F; dout = HID;
-    } else if (f < S::MB * S::KS0 + a.n_hidden * S::MB * S::KSH) {
-      const int g = f - S::MB * S::KS0;
-      layer = 1 + g / (S::MB * S::KSH);
-      const int r = g % (S::MB * S::KSH);
-      mb = r / S::KSH; s = r % S::KSH; ks = S::KSH; din = HID; dout = HID;
-    } else {
-      layer = n_layers - 1; mb = 0; s = f - S::MB * S::KS0 - a.n_hidden * S::MB * S::KSH;
-      ks = S::KSH; din = HID; dout = a.out_dim;
-    }
-    (void)ks;
-    // offset of W_layer inside the decoder's parameter block
-    size_t woff = 0;
-    for (int i = 0; i < layer; ++i) {
-      const int di = i == 0 ? S::F : HID;
-      woff += (size_t)HID * (di + 1);
-    }
-    const int row = mb * 32 + (lane & 31), h = lane >> 5;
-    uint32_t packed[4];
+  const int n_slices = im.n_frags * kWave;
+  for (int base = threadIdx.x; base < n_slices; base += kStageSlices * THREADS) {
+    uint32_t v[kStageSlices][8];
 #pragma unroll
-    for (int e2 = 0; e2 < 4; ++e2) {
-      uint32_t two = 0;
+    for (int i = 0; i < kStageSlices; ++i) {
+      const int lf = base + i * THREADS;
+      const SliceSource<NL, CH, PE, HID> r = slice_source<NL, CH, PE, HID>(a, lf < n_slices ? lf : 0);
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int e = 2 * e2 + j;
-        const int kap = 8 * h + e;
-        const int unit = 16 * s + (layer == 0 ? kap : sigma16(kap));
-        uint16_t v = 0;
-        if (row < dout && unit < din) v = p[woff + (size_t)row * din + unit];
-        two |= (uint32_t)v << (16 * j);
+      for (int e = 0; e < 8; ++e) {
+        const int unit = slice_unit(r, e);
+        const bool in = r.row < r.dout && unit < r.din;
+        const uint32_t off = in ? (uint32_t)(r.woff + (size_t)r.row * r.din + unit) * 2u : kPastBlock;
+        v[i][e] = __builtin_amdgcn_raw_buffer_load_b16(rsrc, off, 0, 0);
       }
-      packed[e2] = two;
     }
-    u32x4 *dst = (u32x4 *)(lds + (size_t)f * 256 + lane * 4);
-    *dst = u32x4{packed[0], packed[1], packed[2], packed[3]};
+#pragma unroll
+    for (int i = 0; i < kStageSlices; ++i) {
+      const int lf = base + i * THREADS;
+      if (lf < n_slices) {
+        const u32x4 packed = {v[i][0] | v[i][1] << 16, v[i][2] | v[i][3] << 16,
+                              v[i][4] | v[i][5] << 16, v[i][6] | v[i][7] << 16};
+        *(u32x4 *)(lds + (size_t)(lf / kWave) * 256 + (lf % kWave) * 4) = packed;
+      }
+    }
   }
-  // biases, converted to fp32; rows past the layer width are zero
+  // biases, converted to fp32; rows past the layer width read zero, as above
+  using S = Shape<NL, CH, PE, HID>;
   float *bias = (float *)(lds + im.bias_off);
   for (int i = threadIdx.x; i < im.n_bias; i += THREADS) {
     int layer, row, dout;
@@ -158,17 +192,12 @@ __device__ void stage_decoder(const DecodeArgs &a, uint32_t dec, uint32_t *lds) 
     } else {
       layer = n_layers - 1; row = i - HID * (1 + a.n_hidden); dout = a.out_dim;
     }
-    size_t off = 0;
-    for (int k = 0; k < layer; ++k) {
-      const int di = k == 0 ? S::F : HID;
-      off += (size_t)HID * (di + 1);
-    }
+    const size_t off =
+        layer == 0 ? 0 : (size_t)HID * (S::F + 1) + (size_t)(layer - 1) * HID * (HID + 1);
     const int din = layer == 0 ? S::F : HID;
-    float v = 0.f;
-    if (row < dout) {
-      const uint16_t hb = p[off + (size_t)dout * din + row];
-      v = (float)__builtin_bit_cast(_Float16, hb);
-    }
+    const uint32_t boff = row < dout ? (uint32_t)(off + (size_t)dout * din + row) * 2u : kPastBlock;
+    const uint16_t hb = __builtin_amdgcn_raw_buffer_load_b16(rsrc, boff, 0, 0);
+    const float v = (float)__builtin_bit_cast(_Float16, hb);
     bias[i] = layer == n_layers - 1 ? v * -kLog2e : v;
   }
 }
