@@ -266,6 +266,58 @@ int ntc_divergence_map(const uint32_t *tex_id, int32_t width, int32_t height, in
                        int32_t block_w, int32_t block_h, uint32_t *map, uint32_t *histogram,
                        int32_t hist_len, uint64_t *totals, void *stream);
 
+/*
+ * Stage 2 of Alg. "Overall texture processing pipeline" (Sec. 3.3): k-means
+ * clustering of one feature vector per texture (the paper clusters CLIP
+ * embeddings of the textures, Stage 1) into m groups; assign[i] = c(i) is then the texture ->
+ * decoder map of ntc_build_bins and ntc_decode, and counts[g] = k_g the size
+ * of group g.  Lloyd's algorithm in float64:
+ *   centroid g starts as the features of texture init[g];
+ *   iteration t: every texture takes the nearest centroid (squared Euclidean
+ *   distance, ties to the lower g); if no label changed (t > 0) the run stops;
+ *   otherwise every centroid becomes the mean of its textures (members summed
+ *   in ascending i, then divided by their count); an empty group keeps its
+ *   centroid.
+ * At most max_iter iterations; ntc_kmeans_result reports how many ran and
+ * whether the labels converged.  A label decided by a near-exact distance tie
+ * may differ from another implementation's.
+ *   features:  f32 [n][dim] (device), row-major
+ *   init:      u32 [m] (HOST), distinct texture indices < n (the seeding is the
+ *              caller's choice; the paper does not state one)
+ *   assign:    u32 [n] (device, output)
+ *   centroids: f64 [m][dim] (device, output)
+ *   counts:    u32 [m] (device, output)
+ *   workspace: >= ntc_kmeans_workspace_bytes(m, max_iter) bytes (device),
+ *              4-byte aligned; holds the iteration state until its next use.
+ * Limits: 1 <= m <= min(n, NTC_MAX_DECODERS); n <= NTC_KMEANS_MAX_POINTS;
+ * dim <= NTC_KMEANS_MAX_DIM; 1 <= max_iter <= NTC_KMEANS_MAX_ITER (else
+ * NTC_ERR_ARG).  Work per iteration is O(n * m * dim) for the assignment and
+ * O(m * n * dim) for the update (one workgroup per group scans all labels).
+ */
+#define NTC_KMEANS_MAX_POINTS (1 << 20)
+#define NTC_KMEANS_MAX_DIM 65536
+#define NTC_KMEANS_MAX_ITER 4096
+size_t ntc_kmeans_workspace_bytes(int32_t m, int32_t max_iter);
+int ntc_kmeans(const float *features, int32_t n, int32_t dim, int32_t m, const uint32_t *init,
+               int32_t max_iter, uint32_t *assign, double *centroids, uint32_t *counts,
+               void *workspace, size_t workspace_bytes, void *stream);
+
+/* (synchronises `stream`) Iterations the last ntc_kmeans on this workspace ran
+ * (the last one found no label change when *converged is 1; otherwise the run
+ * stopped at max_iter).  Either output may be NULL. */
+int ntc_kmeans_result(const void *workspace, int32_t m, int32_t max_iter, int32_t *iterations,
+                      int32_t *converged, void *stream);
+
+/*
+ * (host) Gradual decoder freezing (Sec. 3.2, Alg. SelfFreezeDecoderGradually):
+ * the factor lambda(e) in [0, 1] that scales the shared decoder's updates at
+ * epoch e, 1/2 (1 + cos(pi p)) with p = clamp((e - freeze_start) /
+ * freeze_duration, 0, 1): 1 before the freezing window, a half-cosine down to
+ * 0 across it, 0 after it.  freeze_start = NaN means no freezing (1 always); a
+ * freeze_duration <= 0 freezes at freeze_start.
+ */
+double ntc_freeze_scale(double epoch, double freeze_start, double freeze_duration);
+
 /* (host) Static description of a status code. */
 const char *ntc_status_string(int status);
 

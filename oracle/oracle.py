@@ -173,3 +173,68 @@ def decode(w, subset=None, threads=None, fill=np.nan, leaky_slope=0.0):
 
 def half_to_double(bits: int) -> float:
     return lib().ntc_oracle_half_to_double(bits)
+
+
+# ----------------------------------------------------------------------------- clustering
+
+
+def kmeans(features, init, max_iter=100, history=False):
+    """Stage 2 of Alg. "Overall texture processing pipeline" (Sec. 3.3): k-means of
+    the per-texture feature rows into m = len(init) groups, Lloyd's iteration in
+    float64.  Centroid g starts at the features of texture init[g].  Each iteration
+    labels every texture with its nearest centroid (squared Euclidean distance,
+    the lowest index among equals); when no label changes (after the first
+    iteration) it stops, otherwise each centroid moves to the mean of its
+    textures, summed one texture after another in ascending index; a group left
+    empty keeps its centroid.  Returns (labels, centroids, sizes k_g, iterations,
+    converged) and, with history=True, the within-group sum of squared distances
+    after each assignment."""
+    x = np.asarray(features, dtype=np.float64)
+    n, dim = x.shape
+    seeds = [int(i) for i in init]
+    m = len(seeds)
+    c = x[seeds].copy()
+    labels = np.full(n, -1, dtype=np.int64)
+    inertia = []
+    iterations, converged = max_iter, False
+    for t in range(max_iter):
+        # distances of every texture to every centroid, one texture at a time
+        new = np.empty(n, dtype=np.int64)
+        total = 0.0
+        for i in range(n):
+            d = ((x[i][None, :] - c) ** 2).sum(axis=1)
+            new[i] = int(np.argmin(d))  # first minimum: lowest index among equals
+            total += float(d[new[i]])
+        inertia.append(total)
+        changed = t == 0 or bool(np.any(new != labels))
+        labels = new
+        if not changed:
+            iterations, converged = t + 1, True
+            break
+        for g in range(m):
+            members = np.nonzero(labels == g)[0]
+            if members.size == 0:
+                continue
+            acc = np.zeros(dim, dtype=np.float64)
+            for i in members:  # ascending texture index
+                acc = acc + x[i]
+            c[g] = acc / members.size
+    sizes = np.bincount(labels, minlength=m)
+    out = (labels.astype(np.uint32), c, sizes.astype(np.uint32), iterations, converged)
+    return out + (inertia,) if history else out
+
+
+def freeze_scale(epoch, freeze_start, freeze_duration):
+    """Gradual decoder freezing of Sec. 3.2 (Alg. SelfFreezeDecoderGradually): the
+    decoder's update factor is 1 until the freezing epoch, 0 once the freezing
+    window of freeze_duration epochs has passed, and in between follows half a
+    cosine period from 1 down to 0 over the fraction of the window elapsed.
+    freeze_start None means the decoder is never frozen."""
+    import math
+
+    if freeze_start is None or epoch < freeze_start:
+        return 1.0
+    if epoch >= freeze_start + freeze_duration:
+        return 0.0
+    elapsed = (epoch - freeze_start) / freeze_duration
+    return 0.5 * (1.0 + math.cos(math.pi * elapsed))

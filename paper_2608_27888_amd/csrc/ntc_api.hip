@@ -1,5 +1,9 @@
 // ntc_api.hip -- the extern "C" entry points of libntc: host-side validation,
 // then the kernel launches of ntc_bins.hip, ntc_decode.hip, ntc_divergence.hip.
+#include <algorithm>
+#include <cmath>
+#include <vector>
+
 #include "ntc_internal.h"
 
 using namespace ntc;
@@ -194,6 +198,50 @@ int ntc_divergence_map(const uint32_t *tex_id, int32_t width, int32_t height, in
   return launch_divergence_map(tex_id, width, height, spp, tex_to_dec, n_textures, n_decoders,
                                block_w, block_h, map, histogram, hist_len, totals,
                                (hipStream_t)stream);
+}
+
+size_t ntc_kmeans_workspace_bytes(int32_t m, int32_t max_iter) {
+  if (m < 1 || m > NTC_MAX_DECODERS || max_iter < 1 || max_iter > NTC_KMEANS_MAX_ITER) return 0;
+  return kmeans_workspace_bytes(m, max_iter);
+}
+
+int ntc_kmeans(const float *features, int32_t n, int32_t dim, int32_t m, const uint32_t *init,
+               int32_t max_iter, uint32_t *assign, double *centroids, uint32_t *counts,
+               void *workspace, size_t workspace_bytes, void *stream) {
+  if (!features || !init || !assign || !centroids || !counts || !workspace) return NTC_ERR_ARG;
+  if (n < 1 || n > NTC_KMEANS_MAX_POINTS || dim < 1 || dim > NTC_KMEANS_MAX_DIM || m < 1 ||
+      m > n || m > NTC_MAX_DECODERS || max_iter < 1 || max_iter > NTC_KMEANS_MAX_ITER)
+    return NTC_ERR_ARG;
+  if ((uintptr_t)workspace & 3) return NTC_ERR_ARG;
+  if (workspace_bytes < kmeans_workspace_bytes(m, max_iter)) return NTC_ERR_CAPACITY;
+  std::vector<uint32_t> seeds(init, init + m);  // distinct textures, each < n
+  std::sort(seeds.begin(), seeds.end());
+  if (seeds.back() >= (uint32_t)n || std::adjacent_find(seeds.begin(), seeds.end()) != seeds.end())
+    return NTC_ERR_ARG;
+  return launch_kmeans(features, n, dim, m, init, max_iter, assign, centroids, counts, workspace,
+                       (hipStream_t)stream);
+}
+
+int ntc_kmeans_result(const void *workspace, int32_t m, int32_t max_iter, int32_t *iterations,
+                      int32_t *converged, void *stream) {
+  if (!workspace || m < 1 || m > NTC_MAX_DECODERS || max_iter < 1 ||
+      max_iter > NTC_KMEANS_MAX_ITER)
+    return NTC_ERR_ARG;
+  return read_kmeans_state(workspace, m, max_iter, iterations, converged, (hipStream_t)stream);
+}
+
+double ntc_freeze_scale(double epoch, double freeze_start, double freeze_duration) {
+  if (std::isnan(freeze_start)) return 1.0;  // no freezing scheduled
+  // progress p through the freezing window, clamped to [0, 1]; a window of
+  // zero length freezes at its start
+  double p;
+  if (freeze_duration > 0.0) {
+    p = (epoch - freeze_start) / freeze_duration;
+    p = p < 0.0 ? 0.0 : (p > 1.0 ? 1.0 : p);
+  } else {
+    p = epoch >= freeze_start ? 1.0 : 0.0;
+  }
+  return 0.5 * (1.0 + std::cos(M_PI * p));
 }
 
 }  // extern "C"

@@ -106,6 +106,15 @@ int launch_decode(const DecodeArgs &a, int n_levels, int channels, int feat, int
 int launch_decode_fma(const DecodeArgs &a, int n_levels, int channels, int hidden,
                       hipStream_t stream);
 
+// k-means of per-texture features (ntc_cluster.hip).  Workspace: m seed
+// indices, then one u32 flag per iteration.
+size_t kmeans_workspace_bytes(int32_t m, int32_t max_iter);
+int launch_kmeans(const float *features, int32_t n, int32_t dim, int32_t m, const uint32_t *init,
+                  int32_t max_iter, uint32_t *assign, double *centroids, uint32_t *counts,
+                  void *workspace, hipStream_t stream);
+int read_kmeans_state(const void *workspace, int32_t m, int32_t max_iter, int32_t *iterations,
+                      int32_t *converged, hipStream_t stream);
+
 inline int hip_status(hipError_t e) { return e == hipSuccess ? NTC_OK : NTC_ERR_HIP; }
 
 }  // namespace ntc

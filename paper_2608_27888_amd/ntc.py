@@ -77,8 +77,16 @@ def lib() -> ctypes.CDLL:
                                     ctypes.POINTER(Queries), P, P, i64, i32, P, P, P]
         L.ntc_divergence_stats.argtypes = [P, i64, P, i32, i32, P, i64, i32, P, P, P]
         L.ntc_divergence_map.argtypes = [P, i32, i32, i32, P, i32, i32, i32, i32, P, P, i32, P, P]
+        L.ntc_kmeans_workspace_bytes.argtypes = [i32, i32]
+        L.ntc_kmeans_workspace_bytes.restype = sz
+        L.ntc_kmeans.argtypes = [P, i32, i32, i32, P, i32, P, P, P, P, sz, P]
+        L.ntc_kmeans_result.argtypes = [P, i32, i32, P, P, P]
+        d = ctypes.c_double
+        L.ntc_freeze_scale.argtypes = [d, d, d]
+        L.ntc_freeze_scale.restype = d
         for f in ("ntc_build_bins", "ntc_get_device_error", "ntc_decode", "ntc_decode_ex",
-                  "ntc_divergence_stats", "ntc_divergence_map"):
+                  "ntc_divergence_stats", "ntc_divergence_map", "ntc_kmeans",
+                  "ntc_kmeans_result"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -324,3 +332,46 @@ def divergence_map(tex_id: torch.Tensor, width: int, height: int, tex_to_dec: to
         _ptr(tex_id), width, height, spp, _ptr(tex_to_dec), T, n_decoders, block_w, block_h,
         _ptr(dmap), _ptr(hist), hist_len, _ptr(tot), _stream(stream)))
     return dmap, hist, tot
+
+
+# ----------------------------------------------------------------------------- clustering
+
+
+@dataclass
+class Clusters:
+    assign: torch.Tensor     # int32 [n]: c(i), the texture -> decoder map
+    centroids: torch.Tensor  # float64 [m][dim]
+    counts: torch.Tensor     # int32 [m]: k_g
+    iterations: int
+    converged: bool
+
+
+def kmeans(features: torch.Tensor, init, max_iter: int = 100, stream=None) -> Clusters:
+    """k-means of per-texture feature vectors (float32 [n][dim] on the device) into
+    m = len(init) groups seeded by the textures `init` (host integers); the labels
+    are a texture -> decoder map.  Synchronises to read the iteration count."""
+    if features.dtype != torch.float32 or features.dim() != 2 or not features.is_contiguous():
+        raise ValueError("features must be a contiguous float32 [n][dim] tensor")
+    n, dim = features.shape
+    seeds = np.ascontiguousarray(np.asarray(init, dtype=np.uint32))
+    m = int(seeds.size)
+    dev = features.device
+    assign = torch.empty(n, dtype=torch.int32, device=dev)
+    centroids = torch.empty((m, dim), dtype=torch.float64, device=dev)
+    counts = torch.empty(m, dtype=torch.int32, device=dev)
+    wsb = lib().ntc_kmeans_workspace_bytes(m, int(max_iter))
+    ws = torch.empty(max(wsb, 4), dtype=torch.uint8, device=dev)
+    st = lib().ntc_kmeans(_ptr(features), n, dim, m, seeds.ctypes.data_as(ctypes.c_void_p),
+                          int(max_iter), _ptr(assign), _ptr(centroids), _ptr(counts), _ptr(ws),
+                          wsb, _stream(stream))
+    _check("ntc_kmeans", st)
+    it, conv = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check("ntc_kmeans_result", lib().ntc_kmeans_result(_ptr(ws), m, int(max_iter), ctypes.byref(it),
+                                                        ctypes.byref(conv), _stream(stream)))
+    return Clusters(assign, centroids, counts, int(it.value), bool(conv.value))
+
+
+def freeze_scale(epoch: float, freeze_start: Optional[float], freeze_duration: float) -> float:
+    """Gradual decoder-freezing factor lambda(epoch); freeze_start None = never."""
+    start = float("nan") if freeze_start is None else float(freeze_start)
+    return float(lib().ntc_freeze_scale(float(epoch), start, float(freeze_duration)))

@@ -29,7 +29,8 @@ from typing import Optional
 import numpy as np
 
 # Child-stream indices of the seed sequence, one per drawn component.
-_STREAM_LATENTS, _STREAM_DECODERS, _STREAM_MAP, _STREAM_QUERIES, _STREAM_LAYOUT = range(5)
+(_STREAM_LATENTS, _STREAM_DECODERS, _STREAM_MAP, _STREAM_QUERIES, _STREAM_LAYOUT,
+ _STREAM_FEATURES, _STREAM_SEEDS) = range(7)
 
 F32_BELOW_ONE = np.nextafter(np.float32(1.0), np.float32(0.0))
 
@@ -418,3 +419,32 @@ def small(name: str, seed: int = 0) -> Workload:
     if name in ("k5_per_wave", "k10_per_wave"):
         return k_per_wave(seed, 99, int(name[1:name.index("_")]))
     raise KeyError(name)
+
+
+# ------------------------------------------------------------------ clustering inputs
+
+
+def texture_features(seed: int = 0, n_textures: int = 512, n_groups: int = 16, dim: int = 512,
+                     spread: float = 0.35):
+    """Synthetic stand-ins for the per-texture CLIP embeddings of Stage 1 (Sec. 3.3;
+    the textures and the CLIP model are not available): n_groups "semantic" centres
+    drawn uniformly on the unit sphere of R^dim, group sizes Zipf(1.1) by largest
+    remainder, textures dealt to groups in a seeded random order, and each feature
+    vector its centre plus isotropic noise of norm about `spread`, scaled back to
+    unit length as CLIP embeddings are.  Returns (features float32 [n][dim], the
+    generating group of each texture)."""
+    rng = _rng(seed, _STREAM_FEATURES)
+    centres = rng.standard_normal((n_groups, dim))
+    centres /= np.linalg.norm(centres, axis=1, keepdims=True)
+    sizes = zipf_sizes(n_textures, n_groups, 1.1)
+    group = np.repeat(np.arange(n_groups), sizes)[rng.permutation(n_textures)]
+    f = centres[group] + rng.standard_normal((n_textures, dim)) * (spread / np.sqrt(dim))
+    f /= np.linalg.norm(f, axis=1, keepdims=True)
+    return f.astype(np.float32), group.astype(np.uint32)
+
+
+def kmeans_seeds(seed: int, n_textures: int, m: int) -> np.ndarray:
+    """Seed textures of the clustering: m distinct textures drawn uniformly (the
+    paper does not state a seeding)."""
+    rng = _rng(seed, _STREAM_SEEDS)
+    return np.sort(rng.choice(n_textures, size=m, replace=False)).astype(np.uint32)

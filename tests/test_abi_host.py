@@ -234,3 +234,32 @@ def test_decode_engine_validation(L):
     d.dims[3] = 16
     if not HAS_DEVICE:
         assert call(ntc.NTC_ENGINE_FMA) == ntc.NTC_ERR_HIP
+
+
+def test_kmeans_validation(L):
+    ws = ctypes.c_void_p(0x100000)
+    seeds = (ctypes.c_uint32 * 4)(0, 5, 9, 2)
+    dup = (ctypes.c_uint32 * 4)(0, 5, 5, 2)
+    big = (ctypes.c_uint32 * 4)(0, 5, 10, 2)
+    wsb = L.ntc_kmeans_workspace_bytes(4, 20)
+    assert wsb == (4 + 20) * 4
+    assert L.ntc_kmeans_workspace_bytes(0, 20) == 0
+    assert L.ntc_kmeans_workspace_bytes(4, 0) == 0
+
+    def call(n=10, dim=8, m=4, init=seeds, it=20, ws=ws, wsb=wsb, feats=FAKE):
+        return L.ntc_kmeans(feats, n, dim, m, init, it, FAKE, FAKE, FAKE, ws, wsb, None)
+
+    assert call(feats=None) == ntc.NTC_ERR_ARG
+    assert call(init=None) == ntc.NTC_ERR_ARG
+    assert call(ws=None) == ntc.NTC_ERR_ARG
+    assert call(n=0) == ntc.NTC_ERR_ARG
+    assert call(dim=0) == ntc.NTC_ERR_ARG
+    assert call(n=3) == ntc.NTC_ERR_ARG           # more groups than textures
+    assert call(it=0) == ntc.NTC_ERR_ARG
+    assert call(init=dup) == ntc.NTC_ERR_ARG      # seeds must be distinct
+    assert call(init=big) == ntc.NTC_ERR_ARG      # seed past the last texture
+    assert call(ws=ctypes.c_void_p(0x100002)) == ntc.NTC_ERR_ARG
+    assert call(wsb=wsb - 4) == ntc.NTC_ERR_CAPACITY
+    assert L.ntc_kmeans_result(None, 4, 20, None, None, None) == ntc.NTC_ERR_ARG
+    if not HAS_DEVICE:
+        assert call() == ntc.NTC_ERR_HIP  # valid: its seed copy fails without a device
