@@ -321,6 +321,16 @@ def main():
         result["paper_context"] = ("paper: up to 8.48x (848.49 %) shared vs non-shared WMMA, "
                                    "10 decoders per wave, RX 9070 XT at 1.6 GHz")
         log(f"[bench] compare {result['compare_ms']}")
+    elif not args.no_compare:
+        # one decoder set only (Divergent: one decoder per texture; Single: one
+        # decoder): stream order against the binned step
+        reps = max(3, args.steps // 4)
+        t_stream = timed(lambda: ntc.decode(model, q, None, out=out, stream=stream), reps,
+                         max(2, reps // 2), torch) * 1e3
+        result["compare_ms"] = {f"d{w.n_decoders}_binned": round(ms_step, 4),
+                                f"d{w.n_decoders}_stream": round(t_stream, 4)}
+        result["speedup_stream_vs_binned"] = round(t_stream / ms_step, 3)
+        log(f"[bench] compare {result['compare_ms']}")
 
     # ---------------------------------------------------------------- CPU oracle
     if not args.no_cpu_baseline:
