@@ -120,7 +120,7 @@ def timed(fn, steps, warmup, torch):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the decode path shards by screen slabs with no exchange; see the design notes)",
               file=sys.stderr)
         sys.exit(2)
