@@ -247,13 +247,12 @@ struct Query {
   float u, v, mip;
 };
 
-// Bilinear sample of one level: CH fp32 values, weights in fp32, latents fed
-// to mixed-precision FMAs as fp16.  The lower tap is clamped to [0, res - 2]
-// and the weight to [0, 1]; for res >= 2 this is exactly bilinear filtering
-// with both taps clamped to the edge, and it puts the right-hand tap 2*CH bytes
-// after the left one (an immediate offset) and the lower row res*CH values
-// further on.  Any finite or NaN coordinate keeps every tap inside the level.
 // The 2x2 texels of one level around a query and its position between them.
+// fetch_level clamps the lower tap to [0, res - 2] and the weight to [0, 1]:
+// for res >= 2 this is exactly bilinear filtering with both taps clamped to
+// the edge, and it puts the right-hand tap 2*CH bytes after the left one (an
+// immediate offset) and the lower row res*CH values further on.  Any finite
+// or NaN coordinate keeps every tap inside the level.
 template <int CH>
 struct LevelTaps {
   static constexpr int NV = CH / 8;  // 16-byte vectors per texel
@@ -283,30 +282,11 @@ __device__ __forceinline__ void fetch_level(const uint16_t *tex, uint32_t level_
   }
 }
 
-template <int CH>
-__device__ __forceinline__ void interp_level(const LevelTaps<CH> &L, float *f) {
-  const float gx = 1.f - L.fx, gy = 1.f - L.fy;
-  const float w00 = gx * gy, w10 = L.fx * gy, w01 = gx * L.fy, w11 = L.fx * L.fy;
-#pragma unroll
-  for (int i = 0; i < LevelTaps<CH>::NV; ++i) {
-    const half8 a = as_half8(L.t00[i]), b = as_half8(L.t10[i]);
-    const half8 c = as_half8(L.t01[i]), d = as_half8(L.t11[i]);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float s = __builtin_fmaf(w00, (float)a[e], 0.f);
-      s = __builtin_fmaf(w10, (float)b[e], s);
-      s = __builtin_fmaf(w01, (float)c[e], s);
-      s = __builtin_fmaf(w11, (float)d[e], s);
-      f[8 * i + e] = s;
-    }
-  }
-}
-
-// The same bilinear weights applied in packed fp16: each operation handles a
-// channel pair, the four weights are rounded to fp16 and every product and sum
-// is an fp16 operation (one v_pk_mul_f16 and three v_pk_fma_f16 per pair).
-// This halves the interpolation's instructions; its rounding stays well inside
-// the decode tolerance.  Writes CH / 2 packed pairs, channel order.
+// Bilinear weights applied in packed fp16: each operation handles a channel
+// pair, the four weights are rounded to fp16 and every product and sum is an
+// fp16 operation (one v_pk_mul_f16 and three v_pk_fma_f16 per pair), half the
+// instructions of an fp32 interpolation; its rounding stays well inside the
+// decode tolerance.  Writes CH / 2 packed pairs, channel order.
 __device__ __forceinline__ half2v as_h2(uint32_t v) { return __builtin_bit_cast(half2v, v); }
 
 template <int CH>
@@ -327,20 +307,6 @@ __device__ __forceinline__ void interp_level_h2(const LevelTaps<CH> &L, uint32_t
       xo[4 * i + e] = __builtin_bit_cast(uint32_t, r);
     }
   }
-}
-
-// Bilinear sample of one level: CH fp32 values, weights in fp32, latents fed
-// to mixed-precision FMAs as fp16.  The lower tap is clamped to [0, res - 2]
-// and the weight to [0, 1]; for res >= 2 this is exactly bilinear filtering
-// with both taps clamped to the edge, and it puts the right-hand tap 2*CH bytes
-// after the left one (an immediate offset) and the lower row res*CH values
-// further on.  Any finite or NaN coordinate keeps every tap inside the level.
-template <int CH>
-__device__ __forceinline__ void sample_level(const uint16_t *tex, uint32_t level_off, int res,
-                                             float resf, float u, float v, float *f) {
-  LevelTaps<CH> L;
-  fetch_level<CH>(tex, level_off, res, resf, u, v, L);
-  interp_level<CH>(L, f);
 }
 
 // v[k] for a per-lane level index k < NL, as a chain of selects (no scratch).
@@ -366,23 +332,36 @@ __device__ __forceinline__ void gather(const DecodeArgs &a, const Query &qq,
       fetch_level<CH>(tex, a.level_off[l], a.res[l], a.resf[l], qq.u, qq.v, L);
       interp_level_h2<CH>(L, x + l * CH / 2);
     } else {
-      float f[CH];
-      float m = __builtin_fminf(__builtin_fmaxf(qq.mip, 0.f), (float)(NL - 1));
+      // Each level is interpolated in packed fp16 like the plain path, and the
+      // blend f0 + t (f1 - f0) is one packed subtract and one packed fma per
+      // pair (max-abs error of the decoded channels 9.7e-4 against 7.1e-4 for
+      // an fp32 interpolation, 4 % less decode time on Wide + trilinear).  The
+      // second level is fetched only when some lane of the wave blends: the
+      // coarsest slot never does (its level of detail is always NL - 1).
+      const float m = __builtin_fminf(__builtin_fmaxf(qq.mip, 0.f), (float)(NL - 1));
       const float lod = __builtin_fmaxf((float)l, m);
       const int k0 = (int)__builtin_floorf(lod);
       const int k1 = min(k0 + 1, NL - 1);
       const float t = lod - (float)k0;
-      sample_level<CH>(tex, pick<NL>(a.level_off, k0), pick<NL>(a.res, k0),
-                       pick<NL>(a.resf, k0), qq.u, qq.v, f);
+      LevelTaps<CH> L0;
+      fetch_level<CH>(tex, pick<NL>(a.level_off, k0), pick<NL>(a.res, k0), pick<NL>(a.resf, k0),
+                      qq.u, qq.v, L0);
+      interp_level_h2<CH>(L0, x + l * CH / 2);
       if (__builtin_amdgcn_ballot_w64(t != 0.f)) {
-        float g[CH];
-        sample_level<CH>(tex, pick<NL>(a.level_off, k1), pick<NL>(a.res, k1),
-                         pick<NL>(a.resf, k1), qq.u, qq.v, g);
+        LevelTaps<CH> L1;
+        fetch_level<CH>(tex, pick<NL>(a.level_off, k1), pick<NL>(a.res, k1), pick<NL>(a.resf, k1),
+                        qq.u, qq.v, L1);
+        uint32_t f1[CH / 2];
+        interp_level_h2<CH>(L1, f1);
+        const _Float16 th = (_Float16)t;
+        const half2v t2 = {th, th};
 #pragma unroll
-        for (int c = 0; c < CH; ++c) f[c] = __builtin_fmaf(t, g[c] - f[c], f[c]);
+        for (int c = 0; c < CH / 2; ++c) {
+          const half2v a0 = as_h2(x[l * CH / 2 + c]);
+          x[l * CH / 2 + c] =
+              __builtin_bit_cast(uint32_t, __builtin_elementwise_fma(t2, as_h2(f1[c]) - a0, a0));
+        }
       }
-#pragma unroll
-      for (int c = 0; c < CH; c += 2) x[(l * CH + c) / 2] = pack_half2(f[c], f[c + 1]);
     }
   }
 }
