@@ -24,7 +24,8 @@
  *     between calls.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
  *     device work is enqueued on it and the call returns without waiting,
- *     except ntc_get_device_error, which synchronises the stream.
+ *     except ntc_get_device_error and ntc_kmeans_result, which synchronise
+ *     the stream, and ntc_kmeans, which waits for its copy of a host array.
  *   - Calls on different streams are independent; two calls that share an
  *     output or workspace buffer must be ordered by the caller.
  *   - Arguments are validated on the host before anything is enqueued; on an
@@ -283,7 +284,8 @@ int ntc_divergence_map(const uint32_t *tex_id, int32_t width, int32_t height, in
  * may differ from another implementation's.
  *   features:  f32 [n][dim] (device), row-major
  *   init:      u32 [m] (HOST), distinct texture indices < n (the seeding is the
- *              caller's choice; the paper does not state one)
+ *              caller's choice; the paper does not state one); copied to the
+ *              device before the call returns (the call waits for `stream`)
  *   assign:    u32 [n] (device, output)
  *   centroids: f64 [m][dim] (device, output)
  *   counts:    u32 [m] (device, output)

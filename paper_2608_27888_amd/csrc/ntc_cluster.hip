@@ -98,8 +98,10 @@ int launch_kmeans(const float *features, int32_t n, int32_t dim, int32_t m, cons
                   void *workspace, hipStream_t stream) {
   uint32_t *dinit = (uint32_t *)workspace;  // [m] seed textures, then [max_iter] flags
   uint32_t *flags = dinit + m;
+  // the seed list is the caller's host memory: it is read before this call returns
   if (hipMemcpyAsync(dinit, init, (size_t)m * sizeof(uint32_t), hipMemcpyHostToDevice, stream) !=
-      hipSuccess)
+          hipSuccess ||
+      hipStreamSynchronize(stream) != hipSuccess)
     return NTC_ERR_HIP;
   hipLaunchKernelGGL(kmeans_seed, dim3((unsigned)m), dim3(kBlock), 0, stream, features, dim, dinit,
                      centroids, flags, max_iter);
