@@ -45,6 +45,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float float2v __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
 typedef short short2v __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;
@@ -538,14 +539,17 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_resource(const DecodeArgs 
 }
 
 // How a column block's rows reach memory: for an output width of 4 or 8, one
-// fp32 (or fp16) run of the 4 rows each lane holds; for any other width up to
+// fp32 (or fp16) run of the 4 rows each lane holds; for a width of 3 (RGB rows,
+// the Sec. 4 setup) the lanes holding rows 0..3 store rows 0..2 (fp32: one
+// 12-byte store; fp16: a 4-byte and a 2-byte store); for any other width up to
 // 16, one store per row.
-enum StoreMode { kStoreF32x4 = 0, kStoreF16x4 = 1, kStoreEach = 2 };
+enum StoreMode { kStoreF32x4 = 0, kStoreF16x4 = 1, kStoreEach = 2, kStoreF32x3 = 3,
+                 kStoreF16x3 = 4 };
 
 // Store instructions per 32-query column block; fixed for a mode, so the wait
 // counts of the software pipeline do not depend on the data.
 template <int STORE>
-constexpr int kStoresPerBlock = STORE == kStoreEach ? 8 : 1;
+constexpr int kStoresPerBlock = STORE == kStoreEach ? 8 : STORE == kStoreF16x3 ? 2 : 1;
 
 // Decoded values this lane stores for one 32-query column block: rows 4h..4h+3
 // (lo) and 8+4h..8+4h+3 (hi) of the query in its column, after the sigmoid, as
@@ -606,6 +610,25 @@ __device__ __forceinline__ void store_rows(__amdgpu_buffer_rsrc_t out, int out_d
     const float4 lo = __builtin_bit_cast(float4, r.lo);
     const u32x2 lo16 = {pack_half2(lo.x, lo.y), pack_half2(lo.z, lo.w)};
     __builtin_amdgcn_raw_buffer_store_b64(lo16, out, off, 0, kOutPolicy);
+  } else if constexpr (STORE == kStoreF32x3) {
+    const uint32_t off = ok && h == 0 ? q * 12u : kDropOffset;
+    const u32x3 v = {r.lo[0], r.lo[1], r.lo[2]};
+    __builtin_amdgcn_raw_buffer_store_b96(v, out, off, 0, kOutPolicy);
+  } else if constexpr (STORE == kStoreF16x3) {
+    // the row's 6 bytes start at 6q: for even q the pair (0, 1) is 4-byte
+    // aligned and row 2 follows; for odd q row 0 comes first, then the
+    // aligned pair (1, 2)
+    const float4 lo = __builtin_bit_cast(float4, r.lo);
+    const bool even = (q & 1u) == 0;
+    const uint32_t base = q * 6u;
+    const bool st = ok && h == 0;
+    const uint32_t off32 = st ? (even ? base : base + 2u) : kDropOffset;
+    const uint32_t off16 = st ? (even ? base + 4u : base) : kDropOffset;
+    const uint32_t pair = even ? pack_half2(lo.x, lo.y) : pack_half2(lo.y, lo.z);
+    const _Float16 single = (_Float16)(even ? lo.z : lo.x);
+    __builtin_amdgcn_raw_buffer_store_b32(pair, out, off32, 0, kOutPolicy);
+    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, single), out, off16, 0,
+                                           kOutPolicy);
   } else {
     const uint32_t row = q * (uint32_t)out_dim;
     const uint32_t es = out_f16 ? 2u : 4u;
@@ -944,6 +967,9 @@ int launch_shape(const DecodeArgs &a, hipStream_t stream) {
 
 template <int NL, int CH, int PE, int HID, int NH, bool MIP, bool LEAKY>
 int launch_store(const DecodeArgs &a, hipStream_t stream) {
+  if (a.out_dim == 3)
+    return a.out_f16 ? launch_shape<NL, CH, PE, HID, NH, MIP, kStoreF16x3, LEAKY>(a, stream)
+                     : launch_shape<NL, CH, PE, HID, NH, MIP, kStoreF32x3, LEAKY>(a, stream);
   if (a.out_dim != 4 && a.out_dim != 8)
     return launch_shape<NL, CH, PE, HID, NH, MIP, kStoreEach, LEAKY>(a, stream);
   return a.out_f16 ? launch_shape<NL, CH, PE, HID, NH, MIP, kStoreF16x4, LEAKY>(a, stream)
