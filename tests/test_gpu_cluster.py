@@ -72,10 +72,11 @@ def test_kmeans_hand_worked_and_ties(dev, oracle):
     say("[kmeans] 1-D hand-worked, ties and an empty group, unconverged stop")
     g = check(dev, oracle, np.array([[0.0], [1.0], [10.0], [11.0]], np.float32), [0, 1])
     assert g.assign.tolist() == [0, 0, 1, 1] and g.iterations == 3
-    g = check(dev, oracle, np.array([[0.0], [0.0], [5.0]], np.float32), [0, 1])
+    g = check(dev, oracle, np.array([[1.0], [1.0], [6.0]], np.float32), [0, 1])
     assert g.assign.tolist() == [1, 1, 0]
-    g = check(dev, oracle, np.array([[0.0], [0.0], [5.0]], np.float32), [0, 1], max_iter=1)
+    g = check(dev, oracle, np.array([[1.0], [1.0], [6.0]], np.float32), [0, 1], max_iter=1)
     assert g.counts.tolist() == [3, 0] and not g.converged
+    assert g.centroids[:, 0].tolist() == [8.0 / 3.0, 1.0]  # the empty group kept its seed
 
 
 def test_kmeans_map_drives_the_decode(dev, oracle):

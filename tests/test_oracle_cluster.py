@@ -21,17 +21,18 @@ def test_kmeans_hand_worked_1d():
 
 
 def test_kmeans_ties_and_empty_group():
-    # two seeds at the same point: every distance ties and goes to group 0, which
-    # becomes {0, 0, 5} with mean 5/3 while group 1 is empty and keeps its
-    # centroid 0; then 0 and 0 move to group 1 (0 < 25/9), 5 stays (100/9 < 25).
-    labels, c, sizes, it, conv = O.kmeans(np.array([[0.0], [0.0], [5.0]]), [0, 1])
+    # two seeds on one point (1): every distance ties and goes to group 0, which
+    # becomes {1, 1, 6} with mean 8/3 while group 1 is empty and keeps its
+    # centroid 1; then both 1s move to group 1 (0 < 25/9) and 6 stays
+    # (100/9 < 25); the next iteration changes nothing.
+    labels, c, sizes, it, conv = O.kmeans(np.array([[1.0], [1.0], [6.0]]), [0, 1])
     assert labels.tolist() == [1, 1, 0]
-    assert c[:, 0].tolist() == [5.0, 0.0]
+    assert c[:, 0].tolist() == [6.0, 1.0]
     assert sizes.tolist() == [1, 2] and it == 3 and conv
-    # stopped after one iteration: the tie rule alone decides
-    labels, c, sizes, it, conv = O.kmeans(np.array([[0.0], [0.0], [5.0]]), [0, 1], max_iter=1)
+    # stopped after one iteration: the tie rule and the kept centroid alone decide
+    labels, c, sizes, it, conv = O.kmeans(np.array([[1.0], [1.0], [6.0]]), [0, 1], max_iter=1)
     assert labels.tolist() == [0, 0, 0] and sizes.tolist() == [3, 0]
-    assert c[:, 0].tolist() == [5.0 / 3.0, 0.0] and it == 1 and not conv
+    assert c[:, 0].tolist() == [8.0 / 3.0, 1.0] and it == 1 and not conv
 
 
 def test_kmeans_single_group_is_the_mean():
