@@ -89,19 +89,39 @@ def decode_source_hash() -> str:
     return h.hexdigest()
 
 
-def profiled_traffic(workload: str):
-    """HBM bytes per decode launch from the committed counter profile, or None when the
+COUNTER_PROFILE = os.path.join(ROOT, "profiles", "decode_binned_clustered4k_sq_counters.md")
+
+
+def profile_fields(path: str, workload: str):
+    """The "- key: value" fields of a committed counter profile, or None when the
     profile covers another workload or the decode sources changed since it was taken."""
     try:
-        with open(TRAFFIC_PROFILE) as fh:
+        with open(path) as fh:
             fields = dict(line[2:].split(":", 1) for line in fh if line.startswith("- ") and ":" in line)
     except OSError:
         return None
     fields = {k.strip(): v.strip().strip("`") for k, v in fields.items()}
     if fields.get("workload") != workload or fields.get("decode_source_sha256") != decode_source_hash():
         return None
+    return fields
+
+
+def profiled_traffic(workload: str):
+    """HBM bytes per decode launch from the committed counter profile (FETCH_SIZE and
+    WRITE_SIZE scaled by a device copy's), or None when it does not apply."""
+    fields = profile_fields(TRAFFIC_PROFILE, workload)
     try:
-        return int(fields["traffic_bytes_per_launch"])
+        return int(fields["traffic_bytes_per_launch"]) if fields else None
+    except (KeyError, ValueError):
+        return None
+
+
+def profiled_mfma_busy(workload: str):
+    """MFMA busy cycles over SIMD-cycles (%) of the decode from the committed SQ counter
+    profile, or None when it does not apply."""
+    fields = profile_fields(COUNTER_PROFILE, workload)
+    try:
+        return float(fields["mfma_busy_pct"]) if fields else None
     except (KeyError, ValueError):
         return None
 
@@ -200,6 +220,7 @@ def main():
                 "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     roof["traffic"] = profiled_traffic(w.name)
+    roof["mfma_busy_pct_counters"] = profiled_mfma_busy(w.name)
     roof["kernel"] = "decode_binned"
     roof["algorithmic_bytes_per_launch"] = int(decode_bytes)
     roof["algorithmic_flops_per_launch"] = int(decode_flops)
