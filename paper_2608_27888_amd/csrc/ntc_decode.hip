@@ -929,6 +929,177 @@ decode_stream(const DecodeArgs a) {
   }
 }
 
+// ---------------------------------------------- stream mode, per-wave decoders
+//
+// The stream-mode decode with each wave on its own: a wave evaluates, one
+// after another, the decoders its own tile holds, reading every MFMA A
+// fragment straight from that decoder's parameter block through a raw buffer
+// (rows past the output width read as zero), so there is no workgroup-wide
+// restaging and no barrier.  This is the paper's non-shared tensor decoder
+// (Sec. 4.4): a wave pays one full MLP pass per decoder it holds.  Used for
+// streams over more than one decoder when every decoder block is 16-byte
+// aligned (the fragment loads are 16 and 8 bytes); a single decoder is staged
+// once per workgroup by decode_stream, which then reads its fragments from LDS
+// (on the 4K clustered frame, 16 decoders: 0.74 ms here against 1.81 ms for
+// workgroup restaging; one decoder on an 8192^2 image: 3.2 ms against 1.6 ms).
+//
+// Fragment (layer, row block mb, K-slice s) of lane (row r = 32 mb + lane % 32,
+// half h = lane / 32): layer 0 reads the 8 features 16 s + 8 h .. + 7 of row r
+// (one 16-byte load); later layers read units 16 s + 4 h .. + 3 and
+// 16 s + 8 + 4 h .. + 3 (two 8-byte loads), the order the previous layer's
+// accumulators leave its outputs in (sigma16).
+
+__device__ __forceinline__ half8 load_frag16(__amdgpu_buffer_rsrc_t w, uint32_t off) {
+  return as_half8(__builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(w, off, 0, 0)));
+}
+
+__device__ __forceinline__ half8 load_frag8x2(__amdgpu_buffer_rsrc_t w, uint32_t off) {
+  const u32x2 lo = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(w, off, 0, 0));
+  const u32x2 hi = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(w, off + 16u, 0, 0));
+  return as_half8(u32x4{lo[0], lo[1], hi[0], hi[1]});
+}
+
+// The decoder's biases into this wave's region of LDS (fp32, the image's bias
+// layout: the output layer's rows past its width zero and its biases scaled by
+// -log2(e)); the wave's own earlier reads of the region precede these writes.
+template <int NL, int CH, int PE, int HID>
+__device__ __forceinline__ void stage_biases_wave(const DecodeArgs &a,
+                                                  __amdgpu_buffer_rsrc_t w, float *bias) {
+  using S = Shape<NL, CH, PE, HID>;
+  const int n_layers = a.n_hidden + 2;
+  const int n_bias = HID * (1 + a.n_hidden) + 32;
+  for (int i = lane_id(); i < n_bias; i += kWave) {
+    int layer, row, dout;
+    if (i < HID * (1 + a.n_hidden)) {
+      layer = i / HID; row = i % HID; dout = HID;
+    } else {
+      layer = n_layers - 1; row = i - HID * (1 + a.n_hidden); dout = a.out_dim;
+    }
+    const size_t off =
+        layer == 0 ? 0 : (size_t)HID * (S::F + 1) + (size_t)(layer - 1) * HID * (HID + 1);
+    const int din = layer == 0 ? S::F : HID;
+    const uint32_t boff = row < dout ? (uint32_t)(off + (size_t)dout * din + row) * 2u : kPastBlock;
+    const float v = (float)__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(w, boff, 0, 0));
+    bias[i] = layer == n_layers - 1 ? v * -kLog2e : v;
+  }
+}
+
+// run_mlp with the A fragments from the decoder block `w` and the biases from
+// the wave's LDS region.
+template <int NL, int CH, int PE, int HID, int NH, bool LEAKY>
+__device__ __forceinline__ void run_mlp_direct(__amdgpu_buffer_rsrc_t w, const float *bias,
+                                               int out_dim,
+                                               const half8 (&xb0)[(NL * CH + PE) / 16],
+                                               const half8 (&xb1)[(NL * CH + PE) / 16],
+                                               floatx16 &y0, floatx16 &y1, uint32_t slope_h2) {
+  using S = Shape<NL, CH, PE, HID>;
+  const uint32_t lr = lane_id() & 31u, h = lane_id() >> 5;
+  half8 h0[S::KSH], h1[S::KSH];
+  // layer 0: F -> HID
+#pragma unroll
+  for (int mb = 0; mb < S::MB; ++mb) {
+    floatx16 c0 = bias_frag(bias, mb), c1 = c0;
+    const uint32_t base = ((mb * 32u + lr) * S::F + 8u * h) * 2u;
+#pragma unroll
+    for (int s = 0; s < S::KS0; ++s) {
+      const half8 wf = load_frag16(w, base + 32u * s);
+      c0 = mfma(wf, xb0[s], c0);
+      c1 = mfma(wf, xb1[s], c1);
+    }
+    relu_pack<LEAKY>(c0, h0[2 * mb], h0[2 * mb + 1], slope_h2);
+    relu_pack<LEAKY>(c1, h1[2 * mb], h1[2 * mb + 1], slope_h2);
+  }
+  uint32_t woff = HID * (S::F + 1);
+  const float *bl = bias + HID;
+  // hidden -> hidden
+#pragma unroll
+  for (int layer = 0; layer < NH; ++layer) {
+    half8 n0[S::KSH], n1[S::KSH];
+#pragma unroll
+    for (int mb = 0; mb < S::MB; ++mb) {
+      floatx16 c0 = bias_frag(bl, mb), c1 = c0;
+      const uint32_t base = (woff + (mb * 32u + lr) * HID + 4u * h) * 2u;
+#pragma unroll
+      for (int s = 0; s < S::KSH; ++s) {
+        const half8 wf = load_frag8x2(w, base + 32u * s);
+        c0 = mfma(wf, h0[s], c0);
+        c1 = mfma(wf, h1[s], c1);
+      }
+      relu_pack<LEAKY>(c0, n0[2 * mb], n0[2 * mb + 1], slope_h2);
+      relu_pack<LEAKY>(c1, n1[2 * mb], n1[2 * mb + 1], slope_h2);
+    }
+#pragma unroll
+    for (int s = 0; s < S::KSH; ++s) {
+      h0[s] = n0[s];
+      h1[s] = n1[s];
+    }
+    woff += HID * (HID + 1);
+    bl += HID;
+  }
+  // output layer: rows past the width read zero; bias added by the sigmoid
+  floatx16 c0 = {}, c1 = {};
+  const uint32_t base = lr < (uint32_t)out_dim ? (woff + lr * HID + 4u * h) * 2u : kPastBlock;
+#pragma unroll
+  for (int s = 0; s < S::KSH; ++s) {
+    const half8 wf = load_frag8x2(w, base + 32u * s);
+    c0 = mfma(wf, h0[s], c0);
+    c1 = mfma(wf, h1[s], c1);
+  }
+  y0 = c0;
+  y1 = c1;
+}
+
+template <int NL, int CH, int PE, int HID, int NH, bool MIP, int STORE, bool LEAKY>
+__global__ void __launch_bounds__((kThreads<HID, false>), (kMinBlocks<HID, false>))
+decode_stream_direct(const DecodeArgs a) {
+  constexpr int WAVES = kWaves<HID, false>;
+  using S = Shape<NL, CH, PE, HID>;
+  extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
+  const uint32_t w = threadIdx.x / kWave, lane = lane_id();
+  const int n_bias = HID * (1 + a.n_hidden) + 32;
+  float *bias = (float *)lds + (size_t)w * n_bias;  // this wave's region
+  const __amdgpu_buffer_rsrc_t out_rsrc = out_resource(a);
+  const uint32_t n_tiles = (a.n + kWave - 1) / kWave;
+  const uint32_t per = (n_tiles + gridDim.x * WAVES - 1) / (gridDim.x * WAVES);
+  const uint32_t blk = xcd_local_block(blockIdx.x, gridDim.x);
+  const uint32_t t_begin = (blk * WAVES + w) * per, t_end = min(t_begin + per, n_tiles);
+  const int block_bytes = (int)(a.dec_stride * 2);
+  for (uint32_t t = t_begin; t < t_end; ++t) {
+    const uint32_t q = t * kWave + lane;
+    const Query qq = validate(a, load_query<NL, MIP>(a, q, true));
+    uint32_t dq = 0xFFFFFFFFu;
+    bool live = qq.valid;
+    if (live) {
+      const uint32_t dd = a.tex_to_dec[qq.tex];
+      live = dd < (uint32_t)a.n_decoders;
+      dq = live ? dd : 0xFFFFFFFFu;
+    }
+    uint32_t x[S::F / 2];
+    gather<NL, CH, PE, MIP>(a, qq, x);
+    half8 xb0[S::KS0], xb1[S::KS0];
+    to_b_operands<S::KS0>(x, xb0, xb1);
+    uint64_t todo = ballot(live);
+    while (todo) {
+      const uint32_t d = read_lane(dq, (uint32_t)__builtin_ctzll(todo));
+      const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+          (void *)(a.params + (size_t)d * (size_t)a.dec_stride), 0, block_bytes, 0x00020000);
+      stage_biases_wave<NL, CH, PE, HID>(a, wrs, bias);
+      floatx16 z0, z1;
+      run_mlp_direct<NL, CH, PE, HID, NH, LEAKY>(wrs, bias, a.out_dim, xb0, xb1, z0, z1,
+                                                 a.slope_h2);
+      const float *bo = bias + HID * (1 + NH);  // the output layer's scaled biases
+      OutBias ob;
+      ob.lo = *(const floatx4 *)(bo + 4 * (lane >> 5));
+      ob.hi = STORE == kStoreEach && a.out_dim > 8 ? *(const floatx4 *)(bo + 8 + 4 * (lane >> 5))
+                                                   : ob.lo;
+      const bool mine = live && dq == d;
+      store_tile<STORE>(out_rsrc, a.out_dim, q, mine, finish_rows<STORE>(z0, ob, a.out_dim),
+                        finish_rows<STORE>(z1, ob, a.out_dim), a.out_f16);
+      todo &= ~ballot(mine);
+    }
+  }
+}
+
 template <int NL, int CH, int PE, int HID, int NH, bool MIP, int STORE, bool LEAKY>
 int launch_shape(const DecodeArgs &a, hipStream_t stream) {
   const Image im = image_of<NL, CH, PE, HID>(NH);
@@ -936,6 +1107,24 @@ int launch_shape(const DecodeArgs &a, hipStream_t stream) {
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess)
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (!a.bin_offset && a.n_decoders > 1 && a.dec_stride % 8 == 0 &&
+      ((uintptr_t)a.params & 15) == 0) {
+    // stream mode over several decoders, every block 16-byte aligned: per-wave decoders
+    constexpr int waves = kWaves<HID, false>, threads = waves * kWave;
+    const size_t wlds = (size_t)waves * (HID * (1 + NH) + 32) * sizeof(float);
+    const void *fd = (const void *)decode_stream_direct<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>;
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fd, threads, wlds) != hipSuccess ||
+        per_cu < 1)
+      per_cu = 1;
+    const uint64_t tiles = ((uint64_t)a.n + kWave - 1) / kWave;
+    uint64_t blocks = (tiles + waves - 1) / waves;
+    if (blocks > (uint64_t)cus * per_cu) blocks = (uint64_t)cus * per_cu;
+    if (blocks == 0) return NTC_OK;
+    hipLaunchKernelGGL((decode_stream_direct<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>),
+                       dim3((unsigned)blocks), dim3(threads), wlds, stream, a);
+    return hip_status(hipGetLastError());
+  }
   const void *fn = a.bin_offset ? (const void *)decode_binned<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>
                                 : (const void *)decode_stream<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>;
   if (lds > 64 * 1024) {
