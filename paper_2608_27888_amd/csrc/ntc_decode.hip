@@ -931,17 +931,21 @@ decode_stream(const DecodeArgs a) {
 
 // ---------------------------------------------- stream mode, per-wave decoders
 //
-// The stream-mode decode with each wave on its own: a wave evaluates, one
-// after another, the decoders its own tile holds, reading every MFMA A
-// fragment straight from that decoder's parameter block through a raw buffer
-// (rows past the output width read as zero), so there is no workgroup-wide
-// restaging and no barrier.  This is the paper's non-shared tensor decoder
-// (Sec. 4.4): a wave pays one full MLP pass per decoder it holds.  Used for
-// streams over more than one decoder when every decoder block is 16-byte
-// aligned (the fragment loads are 16 and 8 bytes); a single decoder is staged
-// once per workgroup by decode_stream, which then reads its fragments from LDS
-// (on the 4K clustered frame, 16 decoders: 0.74 ms here against 1.81 ms for
-// workgroup restaging; one decoder on an 8192^2 image: 3.2 ms against 1.6 ms).
+// The stream-mode decode for streams over several decoders.  A workgroup takes
+// groups of consecutive tiles, one per wave, as decode_stream does.  Where every
+// wave of a group holds one and the same decoder, that decoder is staged once
+// in LDS and read from there (it stays staged for the groups after it);
+// elsewhere each wave evaluates, one after another, the decoders its own tile
+// holds, reading every MFMA A fragment straight from that decoder's parameter
+// block through a raw buffer (rows past the output width read as zero), with no
+// restaging and no barrier inside the group.  This is the paper's non-shared
+// tensor decoder (Sec. 4.4): a wave pays one full MLP pass per decoder it
+// holds.  Used when every decoder block is 16-byte aligned (the fragment loads
+// are 16 and 8 bytes).  Restaging the union of a group's decoders in LDS, the
+// only mode of decode_stream, makes every wave wait for every decoder of the
+// group (on the 4K clustered frame, 16 decoders: 1.81 ms against 0.74 ms for
+// per-wave reads); per-wave reads alone are twice as slow as one staged copy
+// when waves share a decoder (3.2 ms against 1.6 ms on an 8192^2 image).
 //
 // Fragment (layer, row block mb, K-slice s) of lane (row r = 32 mb + lane % 32,
 // half h = lane / 32): layer 0 reads the 8 features 16 s + 8 h .. + 7 of row r
@@ -1049,50 +1053,88 @@ __device__ __forceinline__ void run_mlp_direct(__amdgpu_buffer_rsrc_t w, const f
   y1 = c1;
 }
 
+// groups between two votes on the staged decoder of decode_stream_mixed
+constexpr uint32_t kStreamVoteEvery = 8;
+
 template <int NL, int CH, int PE, int HID, int NH, bool MIP, int STORE, bool LEAKY>
 __global__ void __launch_bounds__((kThreads<HID, false>), (kMinBlocks<HID, false>))
-decode_stream_direct(const DecodeArgs a) {
+decode_stream_mixed(const DecodeArgs a, uint32_t image_bytes) {
   constexpr int WAVES = kWaves<HID, false>;
+  constexpr uint32_t kNone = 0xFFFFFFFFu, kMixed = 0xFFFFFFFEu;
   using S = Shape<NL, CH, PE, HID>;
   extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
+  __shared__ uint32_t wave_dec[2][WAVES];
   const uint32_t w = threadIdx.x / kWave, lane = lane_id();
-  const int n_bias = HID * (1 + a.n_hidden) + 32;
-  float *bias = (float *)lds + (size_t)w * n_bias;  // this wave's region
+  constexpr int n_bias = HID * (1 + NH) + 32;
+  float *bias = (float *)(lds + image_bytes / 4) + (size_t)w * n_bias;  // this wave's region
   const __amdgpu_buffer_rsrc_t out_rsrc = out_resource(a);
   const uint32_t n_tiles = (a.n + kWave - 1) / kWave;
-  const uint32_t per = (n_tiles + gridDim.x * WAVES - 1) / (gridDim.x * WAVES);
+  const uint32_t n_groups = (n_tiles + WAVES - 1) / WAVES;
+  const uint32_t per = (n_groups + gridDim.x - 1) / gridDim.x;
   const uint32_t blk = xcd_local_block(blockIdx.x, gridDim.x);
-  const uint32_t t_begin = (blk * WAVES + w) * per, t_end = min(t_begin + per, n_tiles);
+  const uint32_t g_begin = blk * per, g_end = min(g_begin + per, n_groups);
   const int block_bytes = (int)(a.dec_stride * 2);
-  for (uint32_t t = t_begin; t < t_end; ++t) {
-    const uint32_t q = t * kWave + lane;
+  uint32_t staged = kNone;  // the decoder in the shared image; the same in every wave
+  int parity = 0;
+  for (uint32_t g = g_begin; g < g_end; ++g) {
+    const uint32_t q = (g * WAVES + w) * kWave + lane;
     const Query qq = validate(a, load_query<NL, MIP>(a, q, true));
-    uint32_t dq = 0xFFFFFFFFu;
+    uint32_t dq = kNone;
     bool live = qq.valid;
     if (live) {
       const uint32_t dd = a.tex_to_dec[qq.tex];
       live = dd < (uint32_t)a.n_decoders;
-      dq = live ? dd : 0xFFFFFFFFu;
+      dq = live ? dd : kNone;
     }
     uint32_t x[S::F / 2];
     gather<NL, CH, PE, MIP>(a, qq, x);
     half8 xb0[S::KS0], xb1[S::KS0];
     to_b_operands<S::KS0>(x, xb0, xb1);
     uint64_t todo = ballot(live);
+    // the wave's one decoder, kMixed for several, kNone for none
+    if ((g - g_begin) % kStreamVoteEvery == 0) {
+      // the waves vote on the shared copy at every kStreamVoteEvery-th group only and
+      // run on their own in between
+      const uint32_t first = todo ? read_lane(dq, (uint32_t)__builtin_ctzll(todo)) : kNone;
+      const uint32_t mine_one = ballot(live && dq != first) ? kMixed : first;
+      if (lane == 0) wave_dec[parity][w] = mine_one;
+      __syncthreads();  // also: every wave is done with its reads of the staged image
+      uint32_t common = kNone;
+      bool agree = true;
+#pragma unroll
+      for (int k = 0; k < WAVES; ++k) {
+        const uint32_t v = wave_dec[parity][k];
+        if (v == kNone) continue;
+        if (v == kMixed || (common != kNone && v != common)) agree = false;
+        common = v;
+      }
+      parity ^= 1;
+      if (agree && common != kNone && common != staged) {
+        // every wave of the group holds this one decoder: share one staged copy
+        stage_decoder<NL, CH, PE, HID, kThreads<HID, false>>(a, common, lds);
+        __syncthreads();
+        staged = common;
+      }
+    }
     while (todo) {
       const uint32_t d = read_lane(dq, (uint32_t)__builtin_ctzll(todo));
-      const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
-          (void *)(a.params + (size_t)d * (size_t)a.dec_stride), 0, block_bytes, 0x00020000);
-      stage_biases_wave<NL, CH, PE, HID>(a, wrs, bias);
-      floatx16 z0, z1;
-      run_mlp_direct<NL, CH, PE, HID, NH, LEAKY>(wrs, bias, a.out_dim, xb0, xb1, z0, z1,
-                                                 a.slope_h2);
-      const float *bo = bias + HID * (1 + NH);  // the output layer's scaled biases
-      OutBias ob;
-      ob.lo = *(const floatx4 *)(bo + 4 * (lane >> 5));
-      ob.hi = STORE == kStoreEach && a.out_dim > 8 ? *(const floatx4 *)(bo + 8 + 4 * (lane >> 5))
-                                                   : ob.lo;
       const bool mine = live && dq == d;
+      floatx16 z0, z1;
+      OutBias ob;
+      if (d == staged) {
+        run_mlp<NL, CH, PE, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
+        ob = load_out_bias<NL, CH, PE, HID, NH, STORE>(lds, a.out_dim);
+      } else {
+        const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)(a.params + (size_t)d * (size_t)a.dec_stride), 0, block_bytes, 0x00020000);
+        stage_biases_wave<NL, CH, PE, HID>(a, wrs, bias);
+        run_mlp_direct<NL, CH, PE, HID, NH, LEAKY>(wrs, bias, a.out_dim, xb0, xb1, z0, z1,
+                                                   a.slope_h2);
+        const float *bo = bias + HID * (1 + NH);  // the output layer's scaled biases
+        ob.lo = *(const floatx4 *)(bo + 4 * (lane >> 5));
+        ob.hi = STORE == kStoreEach && a.out_dim > 8 ? *(const floatx4 *)(bo + 8 + 4 * (lane >> 5))
+                                                     : ob.lo;
+      }
       store_tile<STORE>(out_rsrc, a.out_dim, q, mine, finish_rows<STORE>(z0, ob, a.out_dim),
                         finish_rows<STORE>(z1, ob, a.out_dim), a.out_f16);
       todo &= ~ballot(mine);
@@ -1109,20 +1151,25 @@ int launch_shape(const DecodeArgs &a, hipStream_t stream) {
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (!a.bin_offset && a.n_decoders > 1 && a.dec_stride % 8 == 0 &&
       ((uintptr_t)a.params & 15) == 0) {
-    // stream mode over several decoders, every block 16-byte aligned: per-wave decoders
+    // stream mode over several decoders, every block 16-byte aligned: a shared staged
+    // decoder where a whole group agrees on one, per-wave fragment reads elsewhere
     constexpr int waves = kWaves<HID, false>, threads = waves * kWave;
-    const size_t wlds = (size_t)waves * (HID * (1 + NH) + 32) * sizeof(float);
-    const void *fd = (const void *)decode_stream_direct<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>;
+    const uint32_t image_bytes = ((uint32_t)im.bytes + 15u) & ~15u;
+    const size_t mlds = image_bytes + (size_t)waves * (HID * (1 + NH) + 32) * sizeof(float);
+    const void *fm = (const void *)decode_stream_mixed<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>;
+    if (mlds > 64 * 1024 &&
+        hipFuncSetAttribute(fm, hipFuncAttributeMaxDynamicSharedMemorySize, (int)mlds) != hipSuccess)
+      return NTC_ERR_HIP;
     int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fd, threads, wlds) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fm, threads, mlds) != hipSuccess ||
         per_cu < 1)
       per_cu = 1;
     const uint64_t tiles = ((uint64_t)a.n + kWave - 1) / kWave;
     uint64_t blocks = (tiles + waves - 1) / waves;
     if (blocks > (uint64_t)cus * per_cu) blocks = (uint64_t)cus * per_cu;
     if (blocks == 0) return NTC_OK;
-    hipLaunchKernelGGL((decode_stream_direct<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>),
-                       dim3((unsigned)blocks), dim3(threads), wlds, stream, a);
+    hipLaunchKernelGGL((decode_stream_mixed<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>),
+                       dim3((unsigned)blocks), dim3(threads), mlds, stream, a, image_bytes);
     return hip_status(hipGetLastError());
   }
   const void *fn = a.bin_offset ? (const void *)decode_binned<NL, CH, PE, HID, NH, MIP, STORE, LEAKY>
