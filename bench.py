@@ -141,7 +141,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the decode path shards by screen slabs with no exchange; see the design notes)",
+              "(on several GPUs each would decode its own screen slab, with no exchange between them)",
               file=sys.stderr)
         sys.exit(2)
     import torch

@@ -15,9 +15,8 @@
  *     decoder c(i);
  *   - Sec. 2: divergence map = number of distinct ids per block, and the metric
  *     of Eq. (normalized_ones_metric).
- * Readings where the paper is silent (sampling convention, activations, level
- * blending, binning order) are the ones listed in the design notes; each is
- * stated again next to the code that takes it.
+ * Where the paper is silent (sampling convention, activations, level blending,
+ * binning order), the reading taken is stated next to the code that takes it.
  */
 #include "ntc_oracle.h"
 
