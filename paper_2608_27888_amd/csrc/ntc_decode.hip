@@ -932,20 +932,21 @@ decode_stream(const DecodeArgs a) {
 // ---------------------------------------------- stream mode, per-wave decoders
 //
 // The stream-mode decode for streams over several decoders.  A workgroup takes
-// groups of consecutive tiles, one per wave, as decode_stream does.  Where every
-// wave of a group holds one and the same decoder, that decoder is staged once
-// in LDS and read from there (it stays staged for the groups after it);
-// elsewhere each wave evaluates, one after another, the decoders its own tile
-// holds, reading every MFMA A fragment straight from that decoder's parameter
-// block through a raw buffer (rows past the output width read as zero), with no
-// restaging and no barrier inside the group.  This is the paper's non-shared
-// tensor decoder (Sec. 4.4): a wave pays one full MLP pass per decoder it
-// holds.  Used when every decoder block is 16-byte aligned (the fragment loads
-// are 16 and 8 bytes).  Restaging the union of a group's decoders in LDS, the
-// only mode of decode_stream, makes every wave wait for every decoder of the
-// group (on the 4K clustered frame, 16 decoders: 1.81 ms against 0.74 ms for
-// per-wave reads); per-wave reads alone are twice as slow as one staged copy
-// when waves share a decoder (3.2 ms against 1.6 ms on an 8192^2 image).
+// groups of consecutive tiles, one per wave, as decode_stream does.  At every
+// kStreamVoteEvery-th group the waves vote: when all of them hold one and the
+// same decoder, it is staged once in LDS, and every wave reads it from there
+// until a later vote stages another.  Any other decoder a wave holds, the wave
+// evaluates on its own, one decoder after another, reading every MFMA A
+// fragment straight from that decoder's parameter block through a raw buffer
+// (rows past the output width read as zero), with no restaging and no barrier.
+// This is the paper's non-shared tensor decoder (Sec. 4.4): a wave pays one
+// full MLP pass per decoder it holds.  Used when every decoder block is 16-byte
+// aligned (the fragment loads are 16 and 8 bytes).  Restaging the union of a
+// group's decoders in LDS, the only mode of decode_stream, makes every wave
+// wait for every decoder of the group (on the 4K clustered frame, 16 decoders:
+// 1.81 ms against 0.74 ms for per-wave reads); per-wave reads alone are twice
+// as slow as one staged copy when waves share a decoder (3.2 ms against 1.6 ms
+// on an 8192^2 image).
 //
 // Fragment (layer, row block mb, K-slice s) of lane (row r = 32 mb + lane % 32,
 // half h = lane / 32): layer 0 reads the 8 features 16 s + 8 h .. + 7 of row r
