@@ -13,10 +13,13 @@
 //
 // The 2-D map takes one wave per screen block, blocks taken in batches whose
 // first 64 samples are loaded together.  The block's samples are walked
-// 64 at a time as one flat range (row segments back to back); each id sets its
-// bit in a wave-private LDS bitmap over the decoder ids, and the lanes whose
-// atomic OR found the bit clear are the first occurrences, counted with a
-// ballot.  The bitmap is cleared after each block.
+// 64 at a time as one flat range (row segments back to back), each chunk's
+// distinct ids peeled with ballots.  A block of at most 64 samples is counted
+// by the peel alone; in a longer one each peeled id sets its bit in a
+// wave-private LDS bitmap over the decoder ids (one atomic OR from one lane),
+// and the ids whose bit was clear are the first occurrences.  The bitmap is
+// cleared after each such block.  (An atomic OR from every lane serialises on
+// one LDS word when the block holds one decoder.)
 #include "ntc_internal.h"
 
 namespace ntc {
@@ -27,6 +30,8 @@ namespace {
 // larger workgroups keep them off the kernel's critical path.
 constexpr int kDivWaves = 16;
 constexpr int kDivBlock = kDivWaves * kWave;
+// At most one workgroup per CU: the final atomics, not the loads, set these kernels' time.
+constexpr uint64_t kDivGroups = 256;
 
 __global__ void divergence_clear(uint64_t *totals) {
   if (threadIdx.x < 4) totals[threadIdx.x] = 0;
@@ -139,7 +144,8 @@ divergence_blocks(const uint32_t *__restrict__ tex_id, uint32_t width, uint32_t 
   // LDS: kDivWaves bitmaps of `words` words, then the workgroup histogram
   extern __shared__ uint32_t lds[];
   __shared__ uint64_t lds_sum[kDivWaves][4];
-  const uint32_t lane = lane_id(), w = threadIdx.x / kWave;
+  const uint32_t lane = lane_id();
+  const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // uniform
   const uint32_t words = (n_decoders + 31) / 32;
   uint32_t *bits = lds + w * words;
   uint32_t *lhist = lds + kDivWaves * words;
@@ -149,18 +155,38 @@ divergence_blocks(const uint32_t *__restrict__ tex_id, uint32_t width, uint32_t 
   const uint32_t stride = gridDim.x * kDivWaves;
   const bool have_t = n_textures > 0;  // tex_to_dec[0] exists
   // Frame index of sample i of block blk (row segments back to back); total =
-  // the block's sample count.  Indexes past the block are never read.
+  // the block's sample count.  Indexes past the block are never read.  The block's
+  // geometry is wave-uniform (scalar); i / seg, per lane, comes from a float
+  // reciprocal corrected by one step each way, exact while i < 2^20 (the estimate
+  // is then within 1/4 of i / seg), else from an integer division.
   auto sample_index = [&](uint32_t blk, uint32_t i, uint32_t &total) -> uint64_t {
     const uint32_t bi = blk / blocks_x, bj = blk % blocks_x;
     const uint32_t x0 = bj * block_w, x1 = min(width, x0 + block_w);
     const uint32_t y0 = bi * block_h, y1 = min(height, y0 + block_h);
     const uint32_t seg = (x1 - x0) * spp;  // samples per row segment
     total = seg * (y1 - y0);
-    const uint32_t y = y0 + i / seg, k = i % seg;
-    return ((uint64_t)y * width + x0) * spp + k;
+    uint32_t r, k;
+    if (total < (1u << 20)) {
+      r = (uint32_t)((float)i * (1.0f / (float)seg));
+      int32_t rem = (int32_t)(i - r * seg);
+      if (rem < 0) {
+        --r;
+        rem += (int32_t)seg;
+      } else if (rem >= (int32_t)seg) {
+        ++r;
+        rem -= (int32_t)seg;
+      }
+      k = (uint32_t)rem;
+    } else {
+      r = i / seg;
+      k = i % seg;
+    }
+    return ((uint64_t)(y0 + r) * width + x0) * spp + k;
   };
   constexpr uint32_t kNoDec = 0xFFFFFFFFu;
-  for (uint32_t first = blockIdx.x * kDivWaves + w; first < n_blocks;
+  // a wave takes kBlkBatch consecutive blocks (neighbours along a block row, which
+  // share the cache lines of their row segments)
+  for (uint32_t first = (blockIdx.x * kDivWaves + w) * kBlkBatch; first < n_blocks;
        first += stride * kBlkBatch) {
     // the first 64 samples of kBlkBatch blocks: every load issued before any is used
     // (sample 0 of the frame stands in for a lane past its block)
@@ -168,7 +194,7 @@ divergence_blocks(const uint32_t *__restrict__ tex_id, uint32_t width, uint32_t 
     bool ok[kBlkBatch];
 #pragma unroll
     for (int j = 0; j < kBlkBatch; ++j) {
-      const uint32_t blk = first + (uint32_t)j * stride;
+      const uint32_t blk = first + (uint32_t)j;
       uint32_t total = 0;
       const uint64_t at = sample_index(blk < n_blocks ? blk : 0, lane, total);
       ok[j] = blk < n_blocks && lane < total;
@@ -182,7 +208,7 @@ divergence_blocks(const uint32_t *__restrict__ tex_id, uint32_t width, uint32_t 
     }
 #pragma unroll
     for (int j = 0; j < kBlkBatch; ++j) {
-      const uint32_t blk = first + (uint32_t)j * stride;
+      const uint32_t blk = first + (uint32_t)j;
       if (blk < n_blocks) {
         uint32_t total = 0;
         (void)sample_index(blk, 0, total);
@@ -200,14 +226,24 @@ divergence_blocks(const uint32_t *__restrict__ tex_id, uint32_t width, uint32_t 
               if (dd < n_decoders) d = dd;
             }
           }
-          bool fresh = false;
-          if (d != kNoDec) {
-            const uint32_t bit = 1u << (d & 31);
-            fresh = (atomicOr(&bits[d >> 5], bit) & bit) == 0;
+          // peel the chunk's distinct ids; a block of one chunk needs no bitmap,
+          // a longer one sets one bit per id and chunk (from one lane)
+          uint64_t todo = ballot(d != kNoDec);
+          while (todo) {
+            const uint32_t dl = read_lane(d, (uint32_t)__builtin_ctzll(todo));
+            todo &= ~ballot(d == dl);
+            if (total <= (uint32_t)kWave) {
+              ++distinct;
+            } else {
+              const uint32_t bit = 1u << (dl & 31);
+              uint32_t old = 0;
+              if (lane == 0) old = atomicOr(&bits[dl >> 5], bit);
+              distinct += (__builtin_amdgcn_readfirstlane(old) & bit) == 0;
+            }
           }
-          distinct += (uint32_t)__builtin_popcountll(ballot(fresh));
         }
-        for (uint32_t k = lane; k < words; k += kWave) bits[k] = 0;
+        if (total > (uint32_t)kWave)
+          for (uint32_t k = lane; k < words; k += kWave) bits[k] = 0;
         if (lane == 0) {
           map[blk] = distinct;
           atomicAdd(&lhist[min(distinct, hist_len - 1)], 1u);
@@ -248,7 +284,7 @@ int launch_divergence_map(const uint32_t *tex_id, int32_t width, int32_t height,
   const size_t lds = ((size_t)kDivWaves * words + (size_t)hist_len) * sizeof(uint32_t);
   const uint64_t per_group = (uint64_t)kDivWaves * kBlkBatch;  // one batch per wave
   uint64_t groups = ((uint64_t)n_blocks + per_group - 1) / per_group;
-  if (groups > 1024) groups = 1024;
+  if (groups > kDivGroups) groups = kDivGroups;
   hipLaunchKernelGGL(divergence_blocks, dim3((unsigned)groups), dim3(kDivBlock), lds, stream, tex_id,
                      (uint32_t)width, (uint32_t)height, (uint32_t)spp, tex_to_dec,
                      (uint32_t)n_textures, (uint32_t)n_decoders, (uint32_t)block_w,
@@ -265,7 +301,7 @@ int launch_divergence(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_
   if (n_windows > 0) {
     const uint64_t per_group = (uint64_t)kDivWaves * kWinBatch;  // one batch per wave
     uint64_t blocks = (n_windows + per_group - 1) / per_group;
-    if (blocks > 1024) blocks = 1024;
+    if (blocks > kDivGroups) blocks = kDivGroups;
     hipLaunchKernelGGL(divergence_windows, dim3((unsigned)blocks), dim3(kDivBlock), 0, stream,
                        tex_id, (uint32_t)n, tex_to_dec, (uint32_t)n_textures,
                        (uint32_t)n_decoders, order, (uint64_t)len, (uint32_t)wave, n_windows,
