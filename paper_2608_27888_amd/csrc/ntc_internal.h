@@ -106,6 +106,14 @@ int launch_decode(const DecodeArgs &a, int n_levels, int channels, int feat, int
 int launch_decode_fma(const DecodeArgs &a, int n_levels, int channels, int hidden,
                       hipStream_t stream);
 
+// The kernels of one decoder shape family (levels, channels per level,
+// positional-encoding features, hidden width), defined in ntc_decode_kernels.h
+// and instantiated once per family in ntc_decode_<family>.hip.
+template <int NL, int CH, int PE, int HID>
+int launch_decode_shape(const DecodeArgs &a, hipStream_t stream);
+template <int NL, int CH, int PE, int HID>
+int launch_decode_fma_shape(const DecodeArgs &a, hipStream_t stream);
+
 // k-means of per-texture features (ntc_cluster.hip).  Workspace: m seed
 // indices, then one u32 flag per iteration.
 size_t kmeans_workspace_bytes(int32_t m, int32_t max_iter);
