@@ -2,8 +2,9 @@
 
 Sampling is checked against torch's grid_sample (bilinear, border padding,
 align_corners=False, float64), against the exact value at texel centres and on
-constant grids.  Level blending by mip is checked against grid_sample of the two
-levels blended by hand.  The MLP is checked against a float64 chain of
+constant grids.  Level blending by mip is checked through properties of the
+linear mipmap filter (single levels at integer mips, continuity, betweenness,
+clamping, affine on constant levels), each against grid_sample of one level.  The MLP is checked against a float64 chain of
 torch.nn.functional.linear, and against zero-weight and identity decoders.
 """
 import numpy as np
@@ -116,21 +117,127 @@ def test_constant_latents_give_constant_output(oracle):
     np.testing.assert_allclose(y[0], h, rtol=0, atol=1e-14)
 
 
-@pytest.mark.parametrize("mipval", [0.0, 1.0, 2.0, 0.25, 1.5, 1.999, 3.7, -1.0])
-def test_mip_blending(oracle, mipval):
-    res, ch = [32, 16, 8], [4, 4, 4]
-    n = 800
-    w = make_workload(res, ch, T=2, dims=[12, 8], D=1, n=n, seed=5, mip=np.full(n, mipval))
+# Level blending by mip (the wide trilinear configuration).  The reading is
+# the linear mipmap filter of the graphics APIs (OpenGL 4.6 core profile,
+# Sec. 8.14.3 "Mipmapping", LINEAR_MIPMAP_LINEAR; Vulkan's
+# VK_SAMPLER_MIPMAP_MODE_LINEAR): the two levels around the level of detail
+# are each filtered bilinearly and mixed by the fractional part of the level
+# of detail, which is clamped to the pyramid; slot l of the feature vector
+# is never finer than level l.  The pins below are properties that filter
+# must have, each checked against grid_sample of single levels; none of them
+# recomputes the blend.
+
+MIP_RES, MIP_CH = [32, 16, 8], [4, 4, 4]
+
+
+def _mip_workload(mipval, n=600, seed=5, latents=None):
+    mip = np.broadcast_to(np.asarray(mipval, np.float32), (n,)).copy()
+    return make_workload(MIP_RES, MIP_CH, T=2, dims=[12, 8], D=1, n=n, seed=seed, mip=mip,
+                         latents=latents)
+
+
+def _slot(f, l):
+    return f[:, 4 * l:4 * l + 4]
+
+
+@pytest.mark.parametrize("k", [0, 1, 2])
+def test_mip_integer_levels_are_single_levels(oracle, k):
+    # at an integer mip k, slot l samples level max(l, k) alone
+    w = _mip_workload(float(k))
     f = oracle.features(w)
-    L = 3
-    m = min(max(float(np.float32(mipval)), 0.0), L - 1)  # the query carries an f32 mip
-    for l in range(L):
+    for l in range(3):
+        ref = grid_sample_level(w, max(l, k), w.tex_id, w.uv)
+        np.testing.assert_allclose(_slot(f, l), ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("k", [1, 2])
+@pytest.mark.parametrize("eps", [1.0 / 64, 1.0 / 1024])
+def test_mip_continuous_at_integer_levels(oracle, k, eps):
+    # approaching level k from either side the finest slot tends to level k's
+    # sample, at a rate set by the difference to the neighbouring level: a
+    # filter weighted the wrong way round, or one that never reaches the next
+    # level, jumps at k
+    lo = _mip_workload(k - eps)
+    f_lo = _slot(oracle.features(lo), 0)
+    a = grid_sample_level(lo, k - 1, lo.tex_id, lo.uv)
+    b = grid_sample_level(lo, k, lo.tex_id, lo.uv)
+    assert np.all(np.abs(f_lo - b) <= eps * np.abs(b - a) + 1e-12)
+    if k < 2:
+        hi = _mip_workload(k + eps)
+        f_hi = _slot(oracle.features(hi), 0)
+        c = grid_sample_level(hi, k + 1, hi.tex_id, hi.uv)
+        assert np.all(np.abs(f_hi - b) <= eps * np.abs(c - b) + 1e-12)
+
+
+@pytest.mark.parametrize("mipval", [0.25, 0.5, 0.999, 1.25, 1.75])
+def test_mip_blend_lies_between_its_levels(oracle, mipval):
+    # a fractional level of detail lies between floor and floor + 1, and the
+    # blended value between the two levels' samples (strictly inside where they
+    # differ)
+    w = _mip_workload(mipval)
+    f = oracle.features(w)
+    m = float(np.float32(mipval))
+    for l in range(3):
         lod = max(l, m)
-        k0 = int(np.floor(lod)); k1 = min(k0 + 1, L - 1); t = lod - k0
+        k0 = int(np.floor(lod))
         a = grid_sample_level(w, k0, w.tex_id, w.uv)
-        b = grid_sample_level(w, k1, w.tex_id, w.uv)
-        ref = a + t * (b - a)
-        np.testing.assert_allclose(f[:, 4 * l:4 * l + 4], ref, rtol=0, atol=1e-12)
+        b = grid_sample_level(w, min(k0 + 1, 2), w.tex_id, w.uv)
+        s = _slot(f, l)
+        assert np.all(s >= np.minimum(a, b) - 1e-12) and np.all(s <= np.maximum(a, b) + 1e-12)
+        if lod != k0:
+            differ = np.abs(a - b) > 1e-9
+            inside = (s > np.minimum(a, b)) & (s < np.maximum(a, b))
+            assert differ.any() and np.all(inside[differ])
+
+
+@pytest.mark.parametrize("mipval", [-3.0, -0.5, 0.0, 0.3, 0.9999, 1.0, 1.5])
+def test_mip_below_a_slot_does_not_change_it(oracle, mipval):
+    # slot l is level l whenever mip <= l: coarser slots are never refined by a
+    # small mip, and negative mips clamp to 0
+    w = _mip_workload(mipval)
+    f = oracle.features(w)
+    m = float(np.float32(mipval))
+    for l in range(3):
+        if m <= l:
+            ref = grid_sample_level(w, l, w.tex_id, w.uv)
+            np.testing.assert_allclose(_slot(f, l), ref, rtol=0, atol=1e-12)
+
+
+def test_mip_beyond_the_pyramid_clamps_to_the_coarsest(oracle):
+    w = _mip_workload(7.5)
+    f = oracle.features(w)
+    ref = grid_sample_level(w, 2, w.tex_id, w.uv)
+    for l in range(3):
+        np.testing.assert_allclose(_slot(f, l), ref, rtol=0, atol=1e-12)
+
+
+def test_mip_on_constant_levels_is_affine_and_monotone(oracle):
+    # levels holding the constants 0, 1, 3: the finest slot is a function of the
+    # mip alone, non-decreasing, affine on each whole level interval (its
+    # quarter points average to the interval's ends) and equal to the
+    # constants at the integers
+    consts = [0.0, 1.0, 3.0]
+    stride = W.texture_stride(MIP_RES, MIP_CH)
+    offs = W.level_offsets(MIP_RES, MIP_CH)
+    lat = np.zeros(2 * stride, np.uint16)
+    for t in range(2):
+        for l, c in enumerate(consts):
+            n_l = MIP_RES[l] ** 2 * MIP_CH[l]
+            lat[t * stride + offs[l]:t * stride + offs[l] + n_l] = np.float16(c).view(np.uint16)
+    mips = np.arange(0, 2.0 + 1e-9, 1.0 / 32)
+    vals = []
+    for m in mips:
+        s = _slot(oracle.features(_mip_workload(m, n=64, latents=lat)), 0)
+        assert np.all(s == s[0, 0])
+        vals.append(s[0, 0])
+    vals = np.array(vals)
+    assert np.all(np.diff(vals) >= 0) and np.all(np.diff(vals)[:32] > 0)
+    for k in range(3):
+        assert vals[32 * k] == consts[k]
+    for k in range(2):
+        q1, mid, q3 = vals[32 * k + 8], vals[32 * k + 16], vals[32 * k + 24]
+        ends = vals[32 * k] + vals[32 * k + 32]
+        assert abs(q1 + q3 - ends) < 1e-12 and abs(2 * mid - ends) < 1e-12
 
 
 def test_mip_zero_equals_no_mip(oracle):
