@@ -36,18 +36,21 @@ def log(*a):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    # about 25 ms of work each: the GPU's clocks take several milliseconds of
-    # sustained load to settle, and short warm-ups time the ramp instead
+    # the clocks are settled before the warm-up (--settle-ms), so a few warm-up
+    # steps suffice
     p.add_argument("--steps", type=int, default=100)
-    p.add_argument("--warmup", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="clustered4k",
                    choices=["clustered4k", "single", "divergent", "wide_trilinear"])
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-compare", action="store_true",
                    help="skip the stream/binned x 16/512-decoder comparison runs")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-sample", type=int, default=1 << 22,
+    p.add_argument("--cpu-sample", type=int, default=1 << 20,
                    help="queries of the frame the CPU oracle decodes")
+    p.add_argument("--settle-ms", type=float, default=400.0,
+                   help="untimed steps run for this much wall time before the warm-up, so the "
+                        "GPU clocks reach their steady state whatever --warmup is")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="first run a plain device-to-device copy of this many MiB three times, "
                         "so that a counter profile of this run also holds the copy's HBM bytes")
@@ -76,7 +79,8 @@ def unique_latent_bytes(w) -> int:
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_binned_clustered4k_hbm_traffic.md")
-DECODE_SOURCES = [os.path.join(ROOT, "paper_2608_27888_amd", "csrc", "ntc_decode.hip")]
+DECODE_SOURCES = [os.path.join(ROOT, "paper_2608_27888_amd", "csrc", f)
+                  for f in ("ntc_decode_kernels.h", "ntc_decode_l2c16.hip")]
 
 
 def decode_source_hash() -> str:
@@ -124,6 +128,55 @@ def profiled_mfma_busy(workload: str):
         return float(fields["mfma_busy_pct"]) if fields else None
     except (KeyError, ValueError):
         return None
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, args, W):
+    """The CPU oracle (float64 C, OpenMP over queries) timed on this host: the
+    median of three runs over a bounded sample of the frame (binning of the whole
+    frame scaled to the sample), plus one single-thread run of the tiny
+    configuration for context."""
+    from oracle import oracle as O
+
+    threads = O.default_threads()
+    n = w.n
+    m = min(n, args.cpu_sample)
+    sub = np.unique(np.linspace(0, n - 1, m).round().astype(np.int64))  # spread over the frame
+    runs = []
+    for _ in range(3):
+        tb = time.perf_counter()
+        O.build_bins(w.tex_id, w.tex_to_dec, w.n_decoders, 64)
+        tb = time.perf_counter() - tb
+        td = time.perf_counter()
+        O.decode(w, subset=sub, threads=threads)
+        td = time.perf_counter() - td
+        runs.append(td + tb * sub.size / n)
+    t_sample = float(np.median(runs))
+    tiny = W.tiny(args.seed)
+    t1 = time.perf_counter()
+    O.build_bins(tiny.tex_id, tiny.tex_to_dec, tiny.n_decoders, 64)
+    O.decode(tiny, threads=1)
+    t1 = time.perf_counter() - t1
+    return {
+        "value": round(sub.size / t_sample / 1e9, 6), "unit": "Gtexel/s", "cores": threads,
+        "kind": "oracle", "cpu": cpu_model(),
+        "runs_s": [round(r, 3) for r in runs],
+        "sample": f"{sub.size} queries evenly spaced over the frame decoded in float64, plus "
+                  f"binning of the whole frame scaled to the sample; median of 3 runs "
+                  f"({t_sample:.2f} s)",
+        "tiny_single_thread": {"queries": tiny.n, "s": round(t1, 3),
+                               "gtexel_s": round(tiny.n / t1 / 1e9, 6)},
+    }
 
 
 def timed(fn, steps, warmup, torch):
@@ -184,6 +237,16 @@ def main():
         if i is not None:
             ev[i][1].record(stream)
 
+    # Clock settling: the GPU needs several milliseconds of sustained load before
+    # its clocks stop ramping; untimed steps for a fixed wall time, then the
+    # warm-up steps, then the timed region.
+    settle_steps = 0
+    t_settle = time.perf_counter()
+    while (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
+        for _ in range(10):
+            step()
+        settle_steps += 10
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -194,7 +257,8 @@ def main():
     wall = time.perf_counter() - t_start
     ms_step = wall * 1e3 / args.steps
     decode_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-    log(f"[bench] step {ms_step:.4f} ms, decode kernel {decode_ms:.4f} ms")
+    log(f"[bench] {settle_steps} settling steps, then step {ms_step:.4f} ms, "
+        f"decode kernel {decode_ms:.4f} ms")
     assert ntc.device_error(bins) == 0
 
     # bins alone, for the breakdown
@@ -355,24 +419,7 @@ def main():
 
     # ---------------------------------------------------------------- CPU oracle
     if not args.no_cpu_baseline:
-        from oracle import oracle as O
-
-        threads = O.default_threads()
-        m = min(n, args.cpu_sample)
-        sub = np.unique(np.linspace(0, n - 1, m).round().astype(np.int64))  # spread over the frame
-        tb = time.perf_counter()
-        O.build_bins(w.tex_id, w.tex_to_dec, w.n_decoders, 64)
-        tb = time.perf_counter() - tb
-        td = time.perf_counter()
-        O.decode(w, subset=sub, threads=threads)
-        td = time.perf_counter() - td
-        t_sample = td + tb * sub.size / n
-        result["cpu_baseline"] = {
-            "value": round(sub.size / t_sample / 1e9, 6), "unit": "Gtexel/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{sub.size} queries evenly spaced over the frame decoded in float64, "
-                      f"plus binning of the whole frame scaled to the sample; "
-                      f"{t_sample:.2f} s"}
+        result["cpu_baseline"] = cpu_baseline(w, args, W)
         log(f"[bench] cpu oracle {result['cpu_baseline']}")
 
     print(json.dumps(result), flush=True)
