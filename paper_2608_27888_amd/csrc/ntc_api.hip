@@ -2,17 +2,60 @@
 // then the kernel launches of ntc_bins.hip, ntc_decode.hip, ntc_divergence.hip.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <vector>
 
 #include "ntc_internal.h"
 
 using namespace ntc;
 
+// Device scratch of ntc_build_bins_noalloc, in place of a caller workspace:
+// one copy per GPU the library runs on, held until the process ends.  In host
+// code `scratch` only names the variable; its device address on the current
+// GPU comes from hipGetSymbolAddress, looked up once per device.
+static __device__ __align__(256) unsigned char scratch[NTC_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 constexpr int64_t kMaxQueries = 0xFFFFFFFELL;  // ids and slots are 32-bit; NTC_PAD reserved
 
 bool pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mutex;
+void *scratch_ptr[kMaxDevices] = {};
+
+// Device address of this GPU's scratch (the current device), or NULL.
+void *device_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (!scratch_ptr[dev]) {
+    void *p = nullptr;
+    size_t bytes = 0;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    if (hipGetSymbolSize(&bytes, HIP_SYMBOL(scratch)) != hipSuccess ||
+        bytes != (size_t)NTC_NOALLOC_SCRATCH_BYTES)
+      return nullptr;
+    scratch_ptr[dev] = p;
+  }
+  return scratch_ptr[dev];
+}
+
+// Host checks shared by ntc_build_bins and ntc_build_bins_noalloc.
+int check_bins_args(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
+                    int32_t n_textures, int32_t n_decoders, int32_t align,
+                    const uint32_t *bin_count, const uint32_t *bin_offset, const uint32_t *perm,
+                    int64_t perm_capacity) {
+  if (n < 0 || n > kMaxQueries || n_textures < 1 || n_decoders < 1 ||
+      n_decoders > NTC_MAX_DECODERS || !pow2(align) || align > NTC_MAX_ALIGN)
+    return NTC_ERR_ARG;
+  if (!tex_to_dec || !bin_count || !bin_offset || (n > 0 && (!tex_id || !perm)))
+    return NTC_ERR_ARG;
+  const int64_t cap = ntc_bins_capacity(n, n_decoders, align);
+  if (perm_capacity < cap || cap > kMaxQueries + 1) return NTC_ERR_CAPACITY;
+  return NTC_OK;
+}
 
 }  // namespace
 
@@ -47,17 +90,28 @@ int ntc_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec
                    uint32_t *bin_count, uint32_t *bin_offset, uint32_t *perm,
                    int64_t perm_capacity, void *workspace, size_t workspace_bytes,
                    void *stream) {
-  if (n < 0 || n > kMaxQueries || n_textures < 1 || n_decoders < 1 ||
-      n_decoders > NTC_MAX_DECODERS || !pow2(align) || align > NTC_MAX_ALIGN)
-    return NTC_ERR_ARG;
-  if (!tex_to_dec || !bin_count || !bin_offset || !workspace || (n > 0 && (!tex_id || !perm)))
-    return NTC_ERR_ARG;
-  if ((uintptr_t)workspace & 15) return NTC_ERR_ARG;
-  const int64_t cap = ntc_bins_capacity(n, n_decoders, align);
-  if (perm_capacity < cap || cap > kMaxQueries + 1) return NTC_ERR_CAPACITY;
+  const int st = check_bins_args(tex_id, n, tex_to_dec, n_textures, n_decoders, align, bin_count,
+                                 bin_offset, perm, perm_capacity);
+  if (st != NTC_OK) return st;
+  if (!workspace || ((uintptr_t)workspace & 15)) return NTC_ERR_ARG;
   if (workspace_bytes < ntc_bins_workspace_bytes(n, n_decoders)) return NTC_ERR_CAPACITY;
   return launch_build_bins(tex_id, n, tex_to_dec, n_textures, n_decoders, align, bin_count,
-                           bin_offset, perm, workspace, (hipStream_t)stream);
+                           bin_offset, perm, workspace, nullptr, (hipStream_t)stream);
+}
+
+int ntc_build_bins_noalloc(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
+                           int32_t n_textures, int32_t n_decoders, int32_t align,
+                           uint32_t *bin_count, uint32_t *bin_offset, uint32_t *perm,
+                           int64_t perm_capacity, uint32_t *n_invalid, void *stream) {
+  const int st = check_bins_args(tex_id, n, tex_to_dec, n_textures, n_decoders, align, bin_count,
+                                 bin_offset, perm, perm_capacity);
+  if (st != NTC_OK) return st;
+  if (ntc_bins_workspace_bytes(n, n_decoders) > (size_t)NTC_NOALLOC_SCRATCH_BYTES)
+    return NTC_ERR_CAPACITY;
+  void *ws = device_scratch();
+  if (!ws) return NTC_ERR_HIP;
+  return launch_build_bins(tex_id, n, tex_to_dec, n_textures, n_decoders, align, bin_count,
+                           bin_offset, perm, ws, n_invalid, (hipStream_t)stream);
 }
 
 int ntc_get_device_error(const void *workspace, uint64_t *n_invalid, void *stream) {

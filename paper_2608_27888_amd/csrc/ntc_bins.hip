@@ -168,7 +168,8 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t &excl, uint32_t *l
 
 __global__ void __launch_bounds__(kBlock)
 bins_scan(uint32_t *__restrict__ hist, uint32_t n_slices, uint32_t n_decoders,
-          uint32_t *__restrict__ bin_count, uint32_t *__restrict__ status) {
+          uint32_t *__restrict__ bin_count, uint32_t *__restrict__ status,
+          uint32_t *__restrict__ invalid_out) {
   __shared__ uint32_t lds_tmp[kWavesPerBlock];
   const uint32_t d = blockIdx.x;  // row; row n_decoders counts invalid queries
   uint32_t *row = hist + (size_t)d * n_slices;
@@ -190,8 +191,12 @@ bins_scan(uint32_t *__restrict__ hist, uint32_t n_slices, uint32_t n_decoders,
     excl += v[k];
   }
   if (threadIdx.x == 0) {
-    if (d < n_decoders) bin_count[d] = total;
-    else status[1] = total;
+    if (d < n_decoders) {
+      bin_count[d] = total;
+    } else {
+      status[1] = total;
+      if (invalid_out) *invalid_out = total;
+    }
   }
 }
 
@@ -309,7 +314,7 @@ static_assert(kTargetBlocks * kWavesPerBlock <= (int64_t)kBlock * kScanPerThread
 int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
                       int32_t n_textures, int32_t n_decoders, int32_t align,
                       uint32_t *bin_count, uint32_t *bin_offset, uint32_t *perm,
-                      void *workspace, hipStream_t stream) {
+                      void *workspace, uint32_t *invalid_out, hipStream_t stream) {
   const BinsLayout L = bins_layout(n, n_decoders);
   uint32_t *status = (uint32_t *)workspace;
   uint32_t *hist = status + kStatusWords;
@@ -325,7 +330,7 @@ int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_
                      (uint32_t)n, tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, n_slices,
                      hist, dec16);
   hipLaunchKernelGGL(bins_scan, dim3(D + 1), dim3(kBlock), 0, stream, hist, n_slices, D,
-                     bin_count, status);
+                     bin_count, status, invalid_out);
   hipLaunchKernelGGL(bins_scatter, dim3((unsigned)L.blocks), dim3(kBlock), lds_scatter, stream,
                      dec16, (uint32_t)n, D, (uint32_t)align, (uint32_t)L.chunk, n_slices, hist,
                      bin_count, bin_offset, perm);

@@ -54,10 +54,12 @@ struct BinsLayout {
 
 BinsLayout bins_layout(int64_t n, int32_t n_decoders);
 
+// workspace: bins_layout(n, n_decoders).bytes, 16-byte aligned; invalid_out
+// (device, may be NULL) also receives the invalid-query count.
 int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
                       int32_t n_textures, int32_t n_decoders, int32_t align,
                       uint32_t *bin_count, uint32_t *bin_offset, uint32_t *perm,
-                      void *workspace, hipStream_t stream);
+                      void *workspace, uint32_t *invalid_out, hipStream_t stream);
 
 size_t bins_status_bytes();
 int read_invalid_count(const void *workspace, uint64_t *n_invalid, hipStream_t stream);

@@ -70,6 +70,7 @@ def lib() -> ctypes.CDLL:
         L.ntc_bins_capacity.argtypes = [i64, i32, i32]
         L.ntc_bins_capacity.restype = i64
         L.ntc_build_bins.argtypes = [P, i64, P, i32, i32, i32, P, P, P, i64, P, sz, P]
+        L.ntc_build_bins_noalloc.argtypes = [P, i64, P, i32, i32, i32, P, P, P, i64, P, P]
         L.ntc_get_device_error.argtypes = [P, P, P]
         L.ntc_decode.argtypes = [ctypes.POINTER(Grids), ctypes.POINTER(Decoders), P,
                                  ctypes.POINTER(Queries), P, P, i64, i32, P, P]
@@ -84,7 +85,7 @@ def lib() -> ctypes.CDLL:
         d = ctypes.c_double
         L.ntc_freeze_scale.argtypes = [d, d, d]
         L.ntc_freeze_scale.restype = d
-        for f in ("ntc_build_bins", "ntc_get_device_error", "ntc_decode", "ntc_decode_ex",
+        for f in ("ntc_build_bins", "ntc_build_bins_noalloc", "ntc_get_device_error", "ntc_decode", "ntc_decode_ex",
                   "ntc_divergence_stats", "ntc_divergence_map", "ntc_kmeans",
                   "ntc_kmeans_result"):
             getattr(L, f).restype = ctypes.c_int
@@ -165,6 +166,23 @@ def build_bins(tex_id: torch.Tensor, tex_to_dec: torch.Tensor, n_decoders: int, 
         _ptr(bins.bin_offset), _ptr(bins.perm), bins.capacity, _ptr(bins.workspace),
         int(bins.workspace.numel()), _stream(stream)))
     return bins
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # NTC_NOALLOC_SCRATCH_BYTES
+
+
+def build_bins_noalloc(tex_id: torch.Tensor, tex_to_dec: torch.Tensor, n_decoders: int,
+                       bin_count: torch.Tensor, bin_offset: torch.Tensor, perm: torch.Tensor,
+                       align: int = 64, n_textures: Optional[int] = None,
+                       n_invalid: Optional[torch.Tensor] = None, stream=None) -> None:
+    """ntc_build_bins_noalloc: binning into caller-owned outputs with the library's
+    own device scratch (no workspace); n_invalid (one int32 on the device, or
+    None) receives the count of queries left out of every bin."""
+    n = int(tex_id.numel())
+    T = int(tex_to_dec.numel()) if n_textures is None else int(n_textures)
+    _check("ntc_build_bins_noalloc", lib().ntc_build_bins_noalloc(
+        _ptr(tex_id), n, _ptr(tex_to_dec), T, n_decoders, align, _ptr(bin_count),
+        _ptr(bin_offset), _ptr(perm), int(perm.numel()), _ptr(n_invalid), _stream(stream)))
 
 
 def device_error(bins: Bins, stream=None) -> int:

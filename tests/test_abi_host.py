@@ -263,3 +263,38 @@ def test_kmeans_validation(L):
     assert L.ntc_kmeans_result(None, 4, 20, None, None, None) == ntc.NTC_ERR_ARG
     if not HAS_DEVICE:
         assert call() == ntc.NTC_ERR_HIP  # valid: its seed copy fails without a device
+
+
+def _bins_noalloc(L, **kw):
+    a = dict(tex_id=FAKE, n=100, tex_to_dec=FAKE, T=4, D=2, align=64, cnt=FAKE, off=FAKE,
+             perm=FAKE, cap=100 + 2 * 63, inv=None)
+    a.update(kw)
+    return L.ntc_build_bins_noalloc(a["tex_id"], a["n"], a["tex_to_dec"], a["T"], a["D"],
+                                    a["align"], a["cnt"], a["off"], a["perm"], a["cap"],
+                                    a["inv"], None)
+
+
+def test_build_bins_noalloc_validation(L):
+    assert _bins_noalloc(L, n=-1) == ntc.NTC_ERR_ARG
+    assert _bins_noalloc(L, tex_id=None) == ntc.NTC_ERR_ARG
+    assert _bins_noalloc(L, perm=None) == ntc.NTC_ERR_ARG
+    assert _bins_noalloc(L, cnt=None) == ntc.NTC_ERR_ARG
+    assert _bins_noalloc(L, D=4097) == ntc.NTC_ERR_ARG
+    assert _bins_noalloc(L, align=48) == ntc.NTC_ERR_ARG
+    assert _bins_noalloc(L, cap=100 + 2 * 63 - 1) == ntc.NTC_ERR_CAPACITY
+    # the scratch bound: the workspace ntc_build_bins would need decides
+    limit = ntc.NOALLOC_SCRATCH_BYTES
+    big = 40_000_000  # 80 MB of 16-bit decoder ids alone
+    assert ntc.workspace_bytes(big, 2) > limit
+    assert _bins_noalloc(L, n=big, cap=ntc.perm_capacity(big, 2)) == ntc.NTC_ERR_CAPACITY
+    # the sizes the header promises fit: a 3840x2160 frame with 3000 decoders at one
+    # sample per pixel, 40 at four
+    assert ntc.workspace_bytes(3840 * 2160, 3000) <= limit
+    assert ntc.workspace_bytes(3840 * 2160 * 4, 40) <= limit
+    assert ntc.workspace_bytes(3840 * 2160 * 4, 64) > limit
+
+
+def test_noalloc_scratch_size_matches_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define NTC_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == ntc.NOALLOC_SCRATCH_BYTES
