@@ -51,6 +51,8 @@ def parse():
     p.add_argument("--settle-ms", type=float, default=400.0,
                    help="untimed steps run for this much wall time before the warm-up, so the "
                         "GPU clocks reach their steady state whatever --warmup is")
+    p.add_argument("--cache-dir", default=os.environ.get("NTC_INPUT_CACHE", ""),
+                   help="directory of the seeded inputs saved as .npy (drawn once, then read)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="first run a plain device-to-device copy of this many MiB three times, "
                         "so that a counter profile of this run also holds the copy's HBM bytes")
@@ -206,7 +208,7 @@ def main():
     dev = torch.device("cuda:0")
     ntc.lib()
     t0 = time.time()
-    w = W.make(args.workload, seed=args.seed)
+    w = W.cached(args.workload, seed=args.seed, cache_dir=args.cache_dir)
     log(f"[bench] workload {w.name}: n={w.n} T={w.n_textures} D={w.n_decoders} dims={w.dims} "
         f"levels={w.res}x{w.channels} ({time.time() - t0:.1f} s to draw)")
     model, q = ntc.upload(w, dev)

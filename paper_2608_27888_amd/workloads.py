@@ -394,6 +394,57 @@ def make(name: str, seed: int = 0, **kw) -> Workload:
     return gens[name](seed=seed, **kw)
 
 
+def cached(name: str, seed: int = 0, cache_dir: Optional[str] = None, **kw) -> Workload:
+    """make(name, seed, **kw) through an on-disk cache of .npy files.
+
+    The key is the workload's name, seed and keyword arguments together with a
+    hash of this module's source, so a changed generator never reads a stale
+    entry.  Arrays are written with numpy.save and read back with numpy.load
+    (no pickling); the scalar fields go to a JSON file.  Without cache_dir this
+    is make().
+    """
+    if not cache_dir:
+        return make(name, seed, **kw)
+    import hashlib
+    import json
+    import os
+
+    with open(__file__, "rb") as fh:
+        src = hashlib.sha256(fh.read()).hexdigest()[:16]
+    key = hashlib.sha256(json.dumps([name, seed, sorted(kw.items()), src]).encode()).hexdigest()[:24]
+    d = os.path.join(cache_dir, f"{name}_s{seed}_{key}")
+    arrays = ("latents", "params", "tex_to_dec", "tex_id", "uv", "mip")
+    meta_path = os.path.join(d, "workload.json")
+    if os.path.exists(meta_path):
+        with open(meta_path) as fh:
+            m = json.load(fh)
+        a = {k: (np.load(os.path.join(d, k + ".npy")) if m["has"][k] else None) for k in arrays}
+        return Workload(m["name"], m["n_textures"], m["res"], m["channels"], a["latents"],
+                        m["n_decoders"], m["dims"], a["params"], a["tex_to_dec"], a["tex_id"],
+                        a["uv"], a["mip"], tuple(m["screen"]) if m["screen"] else None,
+                        m["meta"], m["pe_octaves"])
+    w = make(name, seed, **kw)
+    tmp = d + ".tmp%d" % os.getpid()
+    os.makedirs(tmp, exist_ok=True)
+    for k in arrays:
+        v = getattr(w, k)
+        if v is not None:
+            np.save(os.path.join(tmp, k + ".npy"), v)
+    with open(os.path.join(tmp, "workload.json"), "w") as fh:
+        json.dump({"name": w.name, "n_textures": w.n_textures, "res": list(w.res),
+                   "channels": list(w.channels), "n_decoders": w.n_decoders,
+                   "dims": list(w.dims), "screen": list(w.screen) if w.screen else None,
+                   "meta": w.meta, "pe_octaves": w.pe_octaves,
+                   "has": {k: getattr(w, k) is not None for k in arrays}}, fh)
+    try:
+        os.rename(tmp, d)
+    except OSError:  # another process stored it first
+        import shutil
+
+        shutil.rmtree(tmp, ignore_errors=True)
+    return w
+
+
 def small(name: str, seed: int = 0) -> Workload:
     """Reduced-screen version of a workload: same structure, oracle-friendly size.
 

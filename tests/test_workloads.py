@@ -49,3 +49,24 @@ def test_k_per_wave_has_k_decoders_in_every_wave(oracle, k):
     full = per[: w.n // 64]
     assert np.all(full == k)
     assert w.screen == (96, 96, 1) and w.n == 96 * 96
+
+
+def test_cache_round_trip(tmp_path):
+    a = W.cached("divergent", 3, str(tmp_path), width=131, height=67)
+    b = W.cached("divergent", 3, str(tmp_path), width=131, height=67)
+    ref = W.make("divergent", 3, width=131, height=67)
+    for w in (a, b):
+        for k in ("latents", "params", "tex_to_dec", "tex_id", "uv"):
+            assert np.array_equal(getattr(w, k), getattr(ref, k)), k
+            assert getattr(w, k).dtype == getattr(ref, k).dtype, k
+        assert w.mip is None and w.screen == ref.screen and w.dims == ref.dims
+        assert (w.name, w.n_textures, w.res, w.channels, w.n_decoders) == \
+            (ref.name, ref.n_textures, ref.res, ref.channels, ref.n_decoders)
+    # another seed or size is another entry
+    c = W.cached("divergent", 4, str(tmp_path), width=131, height=67)
+    assert not np.array_equal(c.tex_id, a.tex_id)
+    assert len(list(tmp_path.iterdir())) == 2
+    m = W.cached("wide_trilinear", 0, str(tmp_path), width=17, height=9, spp=2, n_decoders=4,
+                 n_textures=8)
+    assert np.array_equal(m.mip, W.make("wide_trilinear", 0, width=17, height=9, spp=2,
+                                        n_decoders=4, n_textures=8).mip)
