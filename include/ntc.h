@@ -190,6 +190,8 @@ int ntc_get_device_error(const void *workspace, uint64_t *n_invalid, void *strea
  * 128; dims[n_layers] in 1 .. 16; level resolutions in 2 .. 16384;
  * latents of one texture < 2^31 values; output of one call at most
  * 4 GiB - 512 bytes (n * dims[n_layers] * 4 bytes).  Other malformed shapes give NTC_ERR_ARG.
+ * Alignment (NTC_ERR_ARG otherwise, when n > 0): latents 16 bytes (taps are read
+ * as 16-byte pieces), uv 8 bytes, tex_id, mip and out 4 bytes (2 for fp16 rows).
  */
 int ntc_decode(const ntc_grids *grids, const ntc_decoders *decoders,
                const uint32_t *tex_to_dec, const ntc_queries *queries,
@@ -221,6 +223,7 @@ typedef struct {
   int32_t output_format;     /* NTC_OUT_F32 or NTC_OUT_F16 */
   int32_t pe_octaves;        /* positional-encoding octaves K: 0, 4 or 8 */
   int32_t engine;            /* NTC_ENGINE_MFMA or NTC_ENGINE_FMA */
+  int32_t gather;            /* NTC_GATHER_DIRECT or NTC_GATHER_STAGED */
 } ntc_decode_options;
 
 /*
@@ -239,6 +242,23 @@ typedef struct {
  */
 #define NTC_ENGINE_MFMA 0
 #define NTC_ENGINE_FMA 1
+
+/*
+ * Latent gathers (Sec. 1: each query samples its texture's latent grid):
+ *   NTC_GATHER_DIRECT: every lane loads the four bilinear taps of its query
+ *     from memory, level by level (the default, and the faster of the two on
+ *     MI355X).
+ *   NTC_GATHER_STAGED: the taps of a 64-query tile are staged in LDS first.
+ *     A query whose bilinear quad differs from the previous query's in the
+ *     tile leads; each leader's quad is loaded once, by several lanes, into a
+ *     wave-private LDS region (prefetched one tile ahead), and every query
+ *     reads its taps from there.  The MLP then runs on 16x16x32 MFMAs.
+ *     Binned decode with the MFMA engine only, 2 levels, no mip and output
+ *     widths up to 8 (NTC_ERR_UNSUPPORTED otherwise).  Results agree with the
+ *     direct gather within rounding (the MFMA shape differs), not bit for bit.
+ */
+#define NTC_GATHER_DIRECT 0
+#define NTC_GATHER_STAGED 1
 
 /*
  * ntc_decode with options (NULL = ReLU, float rows and the MFMA engine, i.e.

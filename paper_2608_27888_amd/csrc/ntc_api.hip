@@ -131,7 +131,7 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
                   int64_t perm_capacity, int32_t align, const ntc_decode_options *opt,
                   void *out, void *stream) {
   if (!g || !m || !q) return NTC_ERR_ARG;
-  ntc_decode_options o = {NTC_ACT_RELU, 0.f, NTC_OUT_F32, 0, NTC_ENGINE_MFMA};
+  ntc_decode_options o = {NTC_ACT_RELU, 0.f, NTC_OUT_F32, 0, NTC_ENGINE_MFMA, NTC_GATHER_DIRECT};
   if (opt) o = *opt;
   if (o.hidden_activation != NTC_ACT_RELU && o.hidden_activation != NTC_ACT_LEAKY_RELU)
     return NTC_ERR_ARG;
@@ -140,6 +140,7 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
   if (o.output_format != NTC_OUT_F32 && o.output_format != NTC_OUT_F16) return NTC_ERR_ARG;
   if (o.pe_octaves != 0 && o.pe_octaves != 4 && o.pe_octaves != 8) return NTC_ERR_ARG;
   if (o.engine != NTC_ENGINE_MFMA && o.engine != NTC_ENGINE_FMA) return NTC_ERR_ARG;
+  if (o.gather != NTC_GATHER_DIRECT && o.gather != NTC_GATHER_STAGED) return NTC_ERR_ARG;
   const bool fma = o.engine == NTC_ENGINE_FMA;
   const int64_t elem = o.output_format == NTC_OUT_F16 ? 2 : 4;
   if (q->n < 0 || q->n > kMaxQueries) return NTC_ERR_ARG;
@@ -149,6 +150,11 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
     return NTC_ERR_ARG;
   const bool binned = bin_offset != nullptr;
   if (q->n > 0 && (!g->latents || !m->params || !q->tex_id || !q->uv || !out))
+    return NTC_ERR_ARG;
+  // taps are loaded as 16-byte pieces of a texel row, (u, v) as one 8-byte pair
+  if (q->n > 0 && (((uintptr_t)g->latents & 15) || ((uintptr_t)q->uv & 7) ||
+                   ((uintptr_t)q->tex_id & 3) || ((uintptr_t)q->mip & 3) ||
+                   ((uintptr_t)out & (elem - 1))))
     return NTC_ERR_ARG;
   // the FMA engine reads 16-byte weight vectors straight from the parameter block
   if (fma && ((uintptr_t)m->params & 15)) return NTC_ERR_ARG;
@@ -215,6 +221,10 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
   a.slope_h2 = (uint32_t)__builtin_bit_cast(uint16_t, slope) * 0x00010001u;
   a.out_f16 = o.output_format == NTC_OUT_F16;
   a.pe_octaves = o.pe_octaves;
+  a.gather = o.gather;
+  if (o.gather == NTC_GATHER_STAGED &&
+      (fma || !binned || q->mip || L != 2 || out_dim > 8))
+    return NTC_ERR_UNSUPPORTED;
   if (fma) {
     if (binned) return NTC_ERR_UNSUPPORTED;  // per-lane decoders: stream order only
     if (out_dim % 8 != 0) return NTC_ERR_UNSUPPORTED;

@@ -1,6 +1,6 @@
 // ntc_decode_fma.hip -- the per-lane vector-FMA decode engine (NTC_ENGINE_FMA) of every
 // shape family.
-#include "ntc_decode_kernels.h"
+#include "ntc_decode_launch.h"
 
 namespace ntc {
 

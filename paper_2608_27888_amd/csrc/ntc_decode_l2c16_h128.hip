@@ -1,5 +1,5 @@
 // ntc_decode_l2c16_h128.hip -- decode kernels of the shape family: two levels of 16 channels, 128-wide hidden layers.
-#include "ntc_decode_kernels.h"
+#include "ntc_decode_launch.h"
 
 namespace ntc {
 

@@ -1,5 +1,5 @@
 // ntc_decode_l2c16_pe.hip -- decode kernels of the shape family: two levels of 16 channels with 4 or 8 positional octaves (the Sec. 4 setup decoder).
-#include "ntc_decode_kernels.h"
+#include "ntc_decode_launch.h"
 
 namespace ntc {
 

@@ -1,5 +1,5 @@
 // ntc_decode_l2c8.hip -- decode kernels of the shape family: two levels of 8 channels (16 features, the tiny configuration; with 4 or 8 positional octaves).
-#include "ntc_decode_kernels.h"
+#include "ntc_decode_launch.h"
 
 namespace ntc {
 

@@ -1,5 +1,5 @@
 // ntc_decode_l3c16.hip -- decode kernels of the shape family: three levels of 16 channels, 64-wide hidden layers.
-#include "ntc_decode_kernels.h"
+#include "ntc_decode_launch.h"
 
 namespace ntc {
 

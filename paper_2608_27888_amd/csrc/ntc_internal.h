@@ -99,6 +99,7 @@ struct DecodeArgs {
   uint32_t slope_h2;                  // LeakyReLU slope as an fp16 pair
   uint32_t out_f16;                   // output rows: 0 fp32, 1 fp16
   int32_t pe_octaves;                 // positional-encoding octaves (0: none)
+  int32_t gather;                     // NTC_GATHER_DIRECT or NTC_GATHER_STAGED
 };
 
 // Returns NTC_ERR_UNSUPPORTED when no kernel is built for the shape.

@@ -273,24 +273,30 @@ NTC_ACT_RELU, NTC_ACT_LEAKY_RELU = 0, 1
 NTC_OUT_F32, NTC_OUT_F16 = 0, 1
 NTC_ENGINE_MFMA, NTC_ENGINE_FMA = 0, 1
 ENGINES = {"mfma": NTC_ENGINE_MFMA, "fma": NTC_ENGINE_FMA}
+NTC_GATHER_DIRECT, NTC_GATHER_STAGED = 0, 1
+GATHERS = {"direct": NTC_GATHER_DIRECT, "staged": NTC_GATHER_STAGED}
 
 
 class DecodeOptions(ctypes.Structure):
     _fields_ = [("hidden_activation", ctypes.c_int32), ("leaky_slope", ctypes.c_float),
                 ("output_format", ctypes.c_int32), ("pe_octaves", ctypes.c_int32),
-                ("engine", ctypes.c_int32)]
+                ("engine", ctypes.c_int32), ("gather", ctypes.c_int32)]
 
 
 def decode(model: DeviceModel, queries: DeviceQueries, bins: Optional[Bins] = None,
            out: Optional[torch.Tensor] = None, stream=None, leaky_slope: Optional[float] = None,
-           out_dtype: torch.dtype = torch.float32, engine: str = "mfma") -> torch.Tensor:
+           out_dtype: torch.dtype = torch.float32, engine: str = "mfma",
+           gather: str = "direct") -> torch.Tensor:
     """Binned mode when `bins` is given, stream (divergent) mode otherwise.  Hidden
     activation ReLU, or LeakyReLU max(x, slope x) when leaky_slope is given; output
     rows float32 or float16; the model's positional-encoding octaves extend the
     decoder input.  engine "mfma" (tensor path) or "fma" (per-lane vector FMA,
-    stream mode only)."""
+    stream mode only); gather "direct" or "staged" (taps staged in LDS, binned
+    MFMA decode only)."""
     if engine not in ENGINES:
         raise ValueError("engine must be 'mfma' or 'fma'")
+    if gather not in GATHERS:
+        raise ValueError("gather must be 'direct' or 'staged'")
     if out_dtype not in (torch.float32, torch.float16):
         raise ValueError("out_dtype must be float32 or float16")
     if out is None:
@@ -302,7 +308,7 @@ def decode(model: DeviceModel, queries: DeviceQueries, bins: Optional[Bins] = No
     opt = DecodeOptions(NTC_ACT_RELU if leaky_slope is None else NTC_ACT_LEAKY_RELU,
                         0.0 if leaky_slope is None else float(leaky_slope),
                         NTC_OUT_F16 if out_dtype == torch.float16 else NTC_OUT_F32,
-                        int(model.pe_octaves), ENGINES[engine])
+                        int(model.pe_octaves), ENGINES[engine], GATHERS[gather])
     if bins is not None:
         st = lib().ntc_decode_ex(ctypes.byref(g), ctypes.byref(d), _ptr(model.tex_to_dec),
                                  ctypes.byref(q), _ptr(bins.bin_offset), _ptr(bins.perm),

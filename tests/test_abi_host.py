@@ -83,7 +83,7 @@ def test_build_bins_validation(L):
 
 
 def _decode(L, res=(256, 128), ch=(16, 16), dims=(32, 64, 64, 8), n=100, D=4, binned=False,
-            align=64, cap=None, nulls=()):
+            align=64, cap=None, nulls=(), ptrs=None):
     g = ntc.Grids()
     g.n_textures, g.n_levels = 4, len(res)
     for i, (r, c) in enumerate(zip(res, ch)):
@@ -96,11 +96,19 @@ def _decode(L, res=(256, 128), ch=(16, 16), dims=(32, 64, 64, 8), n=100, D=4, bi
     d.params = None if "params" in nulls else FAKE
     q = ntc.Queries()
     q.tex_id, q.uv, q.mip, q.n = FAKE, FAKE, None, n
+    out = None if "out" in nulls else FAKE
+    for k, v in (ptrs or {}).items():
+        if k == "latents":
+            g.latents = v
+        elif k == "out":
+            out = v
+        else:
+            setattr(q, k, v)
     if cap is None:
         cap = ntc.perm_capacity(max(n, 0), D, 64)
     return L.ntc_decode(ctypes.byref(g), ctypes.byref(d), FAKE, ctypes.byref(q),
                         FAKE if binned else None, FAKE if binned else None, cap, align,
-                        None if "out" in nulls else FAKE, None)
+                        out, None)
 
 
 def test_decode_validation(L):
@@ -152,6 +160,64 @@ def test_divergence_map_validation(L):
     assert call(hl=0) == ntc.NTC_ERR_ARG
     assert call(hl=4097) == ntc.NTC_ERR_ARG
     assert call(W=1 << 16, H=1 << 16, spp=2) == ntc.NTC_ERR_ARG
+
+
+def test_decode_pointer_alignment(L):
+    """Taps are 16-byte loads from latents, (u, v) one 8-byte load: misaligned
+    pointers are argument errors, whatever the mode; with no queries nothing is
+    read."""
+    off = lambda b: ctypes.c_void_p(0x100000 + b)  # noqa: E731
+    for binned in (False, True):
+        for b in (2, 4, 8):
+            assert _decode(L, binned=binned, ptrs={"latents": off(b)}) == ntc.NTC_ERR_ARG
+        assert _decode(L, binned=binned, ptrs={"uv": off(4)}) == ntc.NTC_ERR_ARG
+        assert _decode(L, binned=binned, ptrs={"tex_id": off(2)}) == ntc.NTC_ERR_ARG
+        assert _decode(L, binned=binned, ptrs={"mip": off(1)}) == ntc.NTC_ERR_ARG
+        assert _decode(L, binned=binned, ptrs={"out": off(2)}) == ntc.NTC_ERR_ARG
+        assert _decode(L, binned=binned, n=0, ptrs={"latents": off(8)}) == ntc.NTC_OK
+        if not HAS_DEVICE:  # aligned but not 16-byte-multiple offsets are accepted
+            assert _decode(L, binned=binned, ptrs={"latents": off(16), "uv": off(8),
+                                                   "tex_id": off(4), "out": off(4)}) \
+                == ntc.NTC_ERR_HIP
+
+
+def test_decode_gather_validation(L):
+    """The LDS-staged gather: binned MFMA decode of 2 levels without mip and at
+    most 8 output channels; an unknown gather is an argument error."""
+    def call(gather, binned=True, dims=(32, 64, 64, 8), res=(256, 128), ch=(16, 16),
+             engine=ntc.NTC_ENGINE_MFMA, mip=False, n=100):
+        g = ntc.Grids()
+        g.n_textures, g.n_levels = 4, len(res)
+        for i, (r, c) in enumerate(zip(res, ch)):
+            g.res[i], g.channels[i] = r, c
+        g.latents = FAKE
+        d = ntc.Decoders()
+        d.n_decoders, d.n_layers = 4, len(dims) - 1
+        for i, v in enumerate(dims):
+            d.dims[i] = v
+        d.params = FAKE
+        q = ntc.Queries()
+        q.tex_id, q.uv, q.mip, q.n = FAKE, FAKE, FAKE if mip else None, n
+        o = ntc.DecodeOptions(ntc.NTC_ACT_RELU, 0.0, ntc.NTC_OUT_F32, 0, engine, gather)
+        cap = ntc.perm_capacity(n, 4, 64)
+        return L.ntc_decode_ex(ctypes.byref(g), ctypes.byref(d), FAKE, ctypes.byref(q),
+                               FAKE if binned else None, FAKE if binned else None, cap,
+                               64 if binned else 0, ctypes.byref(o), FAKE, None)
+
+    S = ntc.NTC_GATHER_STAGED
+    assert call(2) == ntc.NTC_ERR_ARG
+    assert call(-1) == ntc.NTC_ERR_ARG
+    assert call(S, binned=False) == ntc.NTC_ERR_UNSUPPORTED
+    assert call(S, engine=ntc.NTC_ENGINE_FMA) == ntc.NTC_ERR_UNSUPPORTED
+    assert call(S, mip=True) == ntc.NTC_ERR_UNSUPPORTED
+    assert call(S, dims=(32, 64, 64, 12)) == ntc.NTC_ERR_UNSUPPORTED
+    assert call(S, res=(256, 128, 64), ch=(16, 16, 16), dims=(48, 64, 64, 8)) \
+        == ntc.NTC_ERR_UNSUPPORTED
+    assert call(ntc.NTC_GATHER_DIRECT, dims=(32, 64, 64, 12), n=0) == ntc.NTC_OK
+    if not HAS_DEVICE:  # accepted shapes reach the launch
+        for dims, ch in (((32, 64, 64, 8), (16, 16)), ((16, 64, 64, 3), (8, 8)),
+                         ((32, 128, 128, 5), (16, 16)), ((32, 64, 64, 64, 8), (16, 16))):
+            assert call(S, dims=dims, ch=ch) == ntc.NTC_ERR_HIP
 
 
 def test_decode_options_validation(L):

@@ -219,6 +219,48 @@ def test_decode_variants(dev, oracle, name, dims, slope, dtype):
         assert torch.equal(f32.half().view(torch.int16), out_b.view(torch.int16))
 
 
+@pytest.mark.parametrize("align", [128, 256, 4096])
+def test_decode_binned_other_alignments(dev, oracle, align):
+    """Bins padded to 2, 4 or 64 tiles: the pad tiles hold no queries and are
+    skipped; every row matches the oracle and the align-64 decode bit for bit."""
+    w = small("clustered4k_d512")
+    say(f"[decode align] align={align}")
+    model, q = ntc.upload(w, dev)
+    bins = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders, align=align)
+    out = ntc.decode(model, q, bins)
+    bins64 = ntc.build_bins(q.tex_id, model.tex_to_dec, w.n_decoders)
+    out64 = ntc.decode(model, q, bins64)
+    assert np.abs(out.cpu().numpy().astype(np.float64) - oracle.decode(w)).max() <= TOL
+    assert torch.equal(out.view(torch.int32), out64.view(torch.int32))
+
+
+def test_decode_4096_decoders(dev, oracle):
+    """The largest decoder count: 4096 textures of small grids, each with its own
+    decoder (ids scattered over [0, 4096)), about three queries per bin."""
+    rng = np.random.default_rng(11)
+    T = D = 4096
+    res, ch, dims = [16, 8], [16, 16], [32, 64, 64, 8]
+    n = 3 * T + 17
+    lat = W.draw_latents(11, T, res, ch)
+    params = W.draw_decoders(11, D, dims)
+    t2d = rng.permutation(D).astype(np.uint32)
+    tex = rng.integers(0, T, n).astype(np.uint32)
+    uv = rng.random((n, 2), dtype=np.float32)
+    w = W.Workload("d4096", T, res, ch, lat, D, dims, params, t2d, tex, uv, None)
+    say(f"[decode D=4096] n={n}")
+    model, q = ntc.upload(w, dev)
+    bins = ntc.build_bins(q.tex_id, model.tex_to_dec, D)
+    out_b = ntc.decode(model, q, bins)
+    out_s = ntc.decode(model, q)
+    ref = oracle.decode(w)
+    err = np.abs(out_b.cpu().numpy().astype(np.float64) - ref).max()
+    say(f"    max abs err {err:.3e}")
+    assert err <= TOL
+    assert torch.equal(out_b.view(torch.int32), out_s.view(torch.int32))
+    out_g = ntc.decode(model, q, bins, gather="staged")
+    assert np.abs(out_g.cpu().numpy().astype(np.float64) - ref).max() <= TOL
+
+
 def test_decode_fp16_rows_untouched_for_invalid_queries(dev, oracle):
     w = W.small("tiny").with_dims([16, 64, 64, 3], seed=1)
     w.tex_id = w.tex_id.copy()

@@ -3,8 +3,9 @@ over random sizes, decoder counts (up to the 4096 limit), alignments, wave
 widths, invalid ids and texture layouts; the decode over random combinations
 of every supported decoder shape and variant (levels x channels, hidden width,
 depth, output width, mip blending, LeakyReLU, fp16 rows, small and odd level
-resolutions, uv far outside [0, 1)).  Bins and divergence must be bit-exact,
-decoded channels within 2e-3, stream and binned order bit-identical."""
+resolutions, uv far outside [0, 1)), with the LDS-staged gather where it
+applies.  Bins and divergence must be bit-exact, decoded channels within 2e-3,
+stream and binned order bit-identical."""
 import sys
 
 import numpy as np
@@ -126,3 +127,8 @@ def test_random_decode(dev, oracle, seed):
     if w.out_dim % 8 == 0:
         out_f = ntc.decode(model, q, leaky_slope=slope, out_dtype=dtype, engine="fma")
         assert np.abs(out_f.cpu().numpy().astype(np.float64) - ref).max() <= TOL
+    if len(w.res) == 2 and w.mip is None and w.out_dim <= 8:
+        out_g = ntc.decode(model, q, bins, leaky_slope=slope, out_dtype=dtype, gather="staged")
+        err_g = np.abs(out_g.cpu().numpy().astype(np.float64) - ref).max()
+        say(f"    staged gather max abs err {err_g:.3e}")
+        assert err_g <= TOL
