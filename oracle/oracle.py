@@ -34,11 +34,16 @@ _lib = None
 
 
 def lib():
+    """The oracle library; NTC_ORACLE_LIB names another build of the same source
+    (the sanitizer test loads one built with AddressSanitizer and UBSan)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
-            build(force=False)
-        L = ctypes.CDLL(LIB)
+        path = os.environ.get("NTC_ORACLE_LIB")
+        if not path:
+            if not os.path.exists(LIB):
+                build(force=False)
+            path = LIB
+        L = ctypes.CDLL(path)
         P = ctypes.c_void_p
         i32, i64 = ctypes.c_int32, ctypes.c_int64
         L.ntc_oracle_build_bins.argtypes = [P, i64, P, i32, i32, i32, P, P, P, i64, P]
