@@ -142,10 +142,11 @@ int ntc_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec
  * workspace.  Arguments, results and errors are those of ntc_build_bins,
  * except that:
  *   - the scratch is a static device array of NTC_NOALLOC_SCRATCH_BYTES bytes,
- *     one per GPU the library runs on, held until the process ends; a call that
- *     needs more (ntc_bins_workspace_bytes(n, n_decoders) bytes: a 3840x2160
- *     frame fits with up to 3000 decoders at one sample per pixel and up to 40
- *     at four) returns NTC_ERR_CAPACITY before anything is enqueued;
+ *     one per GPU the library runs on, held until the process ends.  A call
+ *     needs ntc_bins_workspace_bytes(n, n_decoders) bytes of it, which is at
+ *     most 4 MiB + 16 bytes whatever n and n_decoders, so every valid call
+ *     fits; a call that needed more would return NTC_ERR_CAPACITY before
+ *     anything is enqueued;
  *   - n_invalid (device, may be NULL) receives the number of queries left out
  *     of every bin, the count ntc_get_device_error reads for ntc_build_bins;
  *   - every call on one GPU works in that GPU's one scratch array, which keeps
@@ -155,7 +156,7 @@ int ntc_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec
  * It calls no hipMalloc, hipFree or other allocating routine.  Its first call
  * on a device looks up that device's scratch address (NTC_ERR_HIP on failure).
  */
-#define NTC_NOALLOC_SCRATCH_BYTES (64u << 20)
+#define NTC_NOALLOC_SCRATCH_BYTES (5u << 20)
 int ntc_build_bins_noalloc(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
                            int32_t n_textures, int32_t n_decoders, int32_t align,
                            uint32_t *bin_count, uint32_t *bin_offset, uint32_t *perm,

@@ -6,50 +6,50 @@
 // binning itself is not in the paper.
 //
 // The unit of the sort is one wave's contiguous slice of the query stream
-// (slice g = workgroup * 4 + wave).  Three kernels:
-//   hist    : every wave resolves the decoder id of each query of its slice
-//             (tex_to_dec[tex_id[q]]), stores it as a 16-bit id for the
-//             scatter, and counts the ids in a wave-private LDS histogram that
-//             becomes column g of hist[d][g]; row D counts invalid queries.
-//   scan    : workgroup d turns row d into an exclusive prefix over slices and
-//             writes bin_count[d] (row D: the invalid count).
-//   scatter : every workgroup first scans bin_count into the padded bin
-//             offsets (workgroup 0 writes bin_offset, the padding slots are
-//             shared out among the workgroups); then each wave walks its slice
-//             in order with wave-private cursors bin_offset[d] + hist[d][g] and
-//             writes every query to the next slot of its bin.
+// (slice g = workgroup * 4 + wave), processed in batches of kBatchRows rows of
+// 64 queries.  Three kernels:
+//   count : every wave resolves the decoder id of each query of its slice
+//           (tex_to_dec[tex_id[q]]) and counts the ids, which become column g
+//           of hist[d][g]; row D counts invalid queries.
+//   scan  : workgroup d turns row d into its exclusive prefix over slices, in
+//           place, and writes bin_count[d] (row D: the invalid count).
+//   place : every workgroup first scans bin_count into the padded bin offsets
+//           (workgroup 0 writes bin_offset, the padding slots are shared out
+//           among the workgroups); then each wave resolves the ids of its slice
+//           again and writes every query to the next slot of its bin, with
+//           cursors starting at bin_offset[d] + hist[d][g].
 // Inside a 64-query row the lanes that share a decoder id are ranked with a
-// ballot and a lane count, so the order inside a bin is ascending query index
-// and the permutation is unique.  A row whose queries all share the decoder of
-// the previous such row (the common case for screen-coherent material maps)
-// touches no LDS: the wave keeps that decoder's count or cursor in a register.
-// Each lane issues a whole batch of loads (and the batch's map lookups) before
-// it consumes any of them, and fetches the next batch while it counts this one.
+// ballot and a lane count, one pass per distinct id of the row, so the order
+// inside a bin is ascending query index and the permutation is unique.  With at
+// most 63 decoders the wave's counters (count) and cursors (place) live in one
+// register, lane k holding decoder k's, and a row costs no LDS access; with more
+// they live in a wave-private LDS table.  A wave issues the id loads of a whole
+// batch, then all of its map lookups, before it uses any of them.  The decoder
+// ids are not stored between the passes: reading tex_id twice moves as many
+// bytes as writing and reading back 16-bit ids, and leaves the count pass
+// without stores.  Workgroups are numbered XCD by XCD, so the histogram
+// entries of neighbouring slices are written from one L2.
 #include "ntc_internal.h"
 
 namespace ntc {
 namespace {
 
-constexpr int kRowsPerBatch = 8;                                  // rows a wave loads at once
-constexpr int64_t kWaveQuantum = (int64_t)kWave * kRowsPerBatch;  // queries per wave batch
+constexpr int kBatchRows = 16;                                   // rows of 64 per wave batch
+constexpr int64_t kWaveQuantum = (int64_t)kWave * kBatchRows;    // queries per wave batch
 constexpr int64_t kChunkQuantum = kWaveQuantum * kWavesPerBlock;  // chunks are multiples of this
-constexpr int64_t kMinChunk = 2 * kChunkQuantum;                  // queries per workgroup, at least
-constexpr int64_t kTargetBlocks = 1024;
-constexpr uint16_t kInvalid16 = 0xFFFF;                           // 16-bit id of an invalid query
-constexpr uint32_t kOutside = 0xFFFFFFFFu;                        // marks a lane past the slice
-constexpr int kScanPerThread = 16;                                // slices per thread in the row scan
+constexpr int64_t kTargetBlocks = 2048;                          // workgroups, at most
+constexpr int64_t kMaxHistWords = (int64_t)1 << 20;              // slice histograms, at most
+constexpr uint32_t kOutside = 0xFFFFFFFFu;                       // a lane past the slice
+constexpr int kScanThreads = 1024;                               // scan: threads per column
+constexpr int kScanPerThread = 8;                                // scan: slices per thread
+constexpr uint32_t kRegDecoders = kWave - 1;                     // register tables up to here
+
+static_assert(kTargetBlocks * kWavesPerBlock <= (int64_t)kScanThreads * kScanPerThread,
+              "one scan pass covers every slice");
 
 // The workspace starts with kStatusWords status words -- [1] is the invalid
-// query count -- followed by the slice histograms and, from a 16-byte aligned
-// offset, the 16-bit decoder id of every query.
+// query count -- followed by hist[n_decoders + 1][slices].
 constexpr int kStatusWords = 4;
-
-// Decoder id of texture t: n_decoders marks an invalid query.
-__device__ __forceinline__ uint32_t decoder_of(uint32_t t, const uint32_t *tex_to_dec,
-                                               uint32_t n_textures, uint32_t n_decoders) {
-  const uint32_t d = t < n_textures ? tex_to_dec[t] : n_decoders;
-  return d < n_decoders ? d : n_decoders;
-}
 
 // Query range [beg, end) of wave w of workgroup b.
 struct Slice {
@@ -64,101 +64,126 @@ __device__ __forceinline__ Slice slice_of(uint32_t b, uint32_t w, uint64_t chunk
   return Slice{beg, beg + wchunk < cend ? beg + wchunk : cend};
 }
 
-__global__ void __launch_bounds__(kBlock)
-bins_hist(const uint32_t *__restrict__ tex_id, uint32_t n,
-          const uint32_t *__restrict__ tex_to_dec, uint32_t n_textures, uint32_t n_decoders,
-          uint32_t chunk, uint32_t n_slices, uint32_t *__restrict__ hist,
-          uint16_t *__restrict__ dec16) {
-  extern __shared__ uint32_t lds[];  // kWavesPerBlock x (n_decoders + 1) counters
-  const uint32_t b = blockIdx.x, w = threadIdx.x / kWave, lane = lane_id();
-  const uint32_t rows = n_decoders + 1;
-  const Slice sl = slice_of(b, w, chunk, n);
-  // A run of whole rows with one decoder is counted in (run_d, run_n) and
-  // added to the histogram when it ends.
-  uint32_t run_d = kOutside, run_n = 0;
-  // Lanes past the slice load its first id (an unconditional load keeps the
-  // compiler's wait counts exact); the row loop masks them out.
-  auto fetch = [&](uint64_t base, uint32_t (&v)[kRowsPerBatch]) {
+// Decoder ids of the batch of kBatchRows rows starting at query `base` (wave
+// uniform, base < end): lanes at or past `end` get kOutside, invalid queries
+// `invalid`.  Every id load is issued, then every map lookup, before any result
+// is used; the loads are unconditional (clamped into the slice), addressed from
+// one wave-uniform pointer with 32-bit lane offsets.
+__device__ __forceinline__ void load_batch(const uint32_t *__restrict__ tex_id,
+                                           const uint32_t *__restrict__ tex_to_dec,
+                                           uint32_t n_textures, uint32_t n_decoders,
+                                           uint32_t invalid, uint64_t base, uint64_t end,
+                                           uint32_t lane, uint32_t (&d)[kBatchRows]) {
+  const uint32_t *row = tex_id + base;
+  const uint64_t left = end - base;
+  const uint32_t lim = left < (uint64_t)kWaveQuantum ? (uint32_t)left : (uint32_t)kWaveQuantum;
 #pragma unroll
-    for (int j = 0; j < kRowsPerBatch; ++j) {
-      const uint64_t q = base + (uint64_t)j * kWave + lane;
-      v[j] = tex_id[q < sl.end ? q : sl.beg];
-    }
-  };
-  // the first batch is in flight while the histogram is cleared
-  uint32_t nxt[kRowsPerBatch];
-  if (sl.beg < sl.end) fetch(sl.beg, nxt);
-  for (uint32_t i = threadIdx.x; i < kWavesPerBlock * rows; i += kBlock) lds[i] = 0;
-  __syncthreads();
-  uint32_t *h = lds + w * rows;
-  for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
-    uint32_t t[kRowsPerBatch];
-#pragma unroll
-    for (int j = 0; j < kRowsPerBatch; ++j) t[j] = nxt[j];
-    // Every row's map lookup is issued before any of them is used: the loads
-    // are unconditional (texture 0 stands in for an out-of-range id or a lane
-    // past the slice), so they are not serialised behind per-row branches.
-    // They go out before the next batch's ids, so that waiting for them does
-    // not wait for that prefetch (loads complete in issue order for the
-    // wait counter).
-    uint32_t m[kRowsPerBatch];
-#pragma unroll
-    for (int j = 0; j < kRowsPerBatch; ++j) m[j] = tex_to_dec[t[j] < n_textures ? t[j] : 0u];
-    __builtin_amdgcn_sched_barrier(0);
-    if (base + kWaveQuantum < sl.end) fetch(base + kWaveQuantum, nxt);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int j = 0; j < kRowsPerBatch; ++j) {
-      const uint64_t q = base + (uint64_t)j * kWave + lane;
-      const bool inside = q < sl.end;
-      const uint32_t d = !inside ? kOutside
-                         : (t[j] < n_textures && m[j] < n_decoders) ? m[j] : n_decoders;
-      if (inside) dec16[q] = d < n_decoders ? (uint16_t)d : kInvalid16;
-      const uint32_t v0 = __builtin_amdgcn_readfirstlane(d);
-      if (ballot(d == v0) == ~0ull) {
-        if (v0 != kOutside) {
-          if (v0 != run_d) {
-            if (run_n && lane == 0) atomicAdd(&h[run_d], run_n);
-            run_d = v0;
-            run_n = 0;
-          }
-          run_n += kWave;
-        }
-      } else {
-        uint64_t todo = ballot(inside);
-        while (todo) {
-          const uint32_t leader = (uint32_t)__builtin_ctzll(todo);
-          const uint32_t dl = read_lane(d, leader);
-          const uint64_t same = ballot(d == dl) & todo;
-          if (lane == leader) atomicAdd(&h[dl], (uint32_t)__builtin_popcountll(same));
-          todo &= ~same;
-        }
-      }
-    }
+  for (int j = 0; j < kBatchRows; ++j) {
+    const uint32_t o = (uint32_t)j * kWave + lane;
+    d[j] = row[o < lim - 1 ? o : lim - 1];
   }
-  if (run_n && lane == 0) atomicAdd(&h[run_d], run_n);
-  __syncthreads();
-  for (uint32_t i = threadIdx.x; i < kWavesPerBlock * rows; i += kBlock) {
-    const uint32_t ww = i / rows, d = i % rows;
-    hist[(size_t)d * n_slices + b * kWavesPerBlock + ww] = lds[i];
+  uint32_t m[kBatchRows];
+#pragma unroll
+  for (int j = 0; j < kBatchRows; ++j) m[j] = tex_to_dec[d[j] < n_textures ? d[j] : 0u];
+#pragma unroll
+  for (int j = 0; j < kBatchRows; ++j) {
+    const uint32_t o = (uint32_t)j * kWave + lane;
+    d[j] = o >= lim ? kOutside : d[j] < n_textures && m[j] < n_decoders ? m[j] : invalid;
   }
 }
 
-// Exclusive scan of the kBlock values held one per thread; returns the total.
-__device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t &excl, uint32_t *lds_tmp) {
+// Table of one value per decoder: lane k of a register (REG) or word k of a
+// wave-private LDS array.
+template <bool REG>
+struct WaveTable {
+  uint32_t reg;
+  uint32_t *lds;
+  // value of decoder dl (wave uniform)
+  __device__ __forceinline__ uint32_t get(uint32_t dl) const {
+    if constexpr (REG) return __builtin_amdgcn_readlane(reg, dl);
+    else return lds[dl];
+  }
+  // adds c to decoder dl's value (called by every lane; `leader` is one lane):
+  // a no-return LDS atomic does not wait for the old value
+  __device__ __forceinline__ void add(uint32_t dl, uint32_t c, uint32_t lane, bool leader) {
+    if constexpr (REG) reg += lane == dl ? c : 0u;
+    else if (leader) atomicAdd(&lds[dl], c);
+  }
+};
+
+// Ranks the valid lanes of one row (d != kOutside) by decoder: each lane gets
+// the table value of its decoder plus the number of lanes below it with the same
+// decoder, and the table advances by the row's count of each decoder.
+template <bool REG, bool RANK>
+__device__ __forceinline__ uint32_t rank_row(uint32_t d, WaveTable<REG> &t, uint32_t lane) {
+  uint64_t todo = ballot(d != kOutside);
+  uint32_t pos = 0;
+  while (todo) {
+    const uint32_t leader = (uint32_t)__builtin_ctzll(todo);
+    const uint32_t dl = read_lane(d, leader);
+    const uint64_t same = ballot(d == dl) & todo;
+    if constexpr (RANK) {
+      const uint32_t at = t.get(dl);
+      pos = d == dl ? at + lanes_below(same) : pos;
+    }
+    t.add(dl, (uint32_t)__builtin_popcountll(same), lane, lane == leader);
+    todo &= ~same;
+  }
+  return pos;
+}
+
+template <bool REG>
+__global__ void __launch_bounds__(kBlock)
+bins_count(const uint32_t *__restrict__ tex_id, uint32_t n,
+           const uint32_t *__restrict__ tex_to_dec, uint32_t n_textures, uint32_t n_decoders,
+           uint32_t chunk, uint32_t *__restrict__ hist) {
+  extern __shared__ uint32_t lds[];  // !REG: kWavesPerBlock x (n_decoders + 1) counters
+  const uint32_t b = xcd_local_block(blockIdx.x, gridDim.x), lane = lane_id();
+  const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const uint32_t cols = n_decoders + 1, n_slices = gridDim.x * kWavesPerBlock;
+  const Slice sl = slice_of(b, w, chunk, n);
+  WaveTable<REG> h{0u, lds + w * cols};
+  if constexpr (!REG)
+    for (uint32_t i = lane; i < cols; i += kWave) h.lds[i] = 0;
+  for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
+    uint32_t d[kBatchRows];
+    load_batch(tex_id, tex_to_dec, n_textures, n_decoders, n_decoders, base, sl.end, lane, d);
+#pragma unroll
+    for (int j = 0; j < kBatchRows; ++j) rank_row<REG, false>(d[j], h, lane);
+  }
+  if constexpr (REG) {
+    // the wave's table is its own: no workgroup barrier
+    if (lane < cols) hist[(size_t)lane * n_slices + b * kWavesPerBlock + w] = h.reg;
+  } else {
+    // the workgroup's kWavesPerBlock slices are neighbours in every row of hist:
+    // thread t writes row t / 4, slice t % 4, so a wave covers 16 rows with
+    // 16-byte pieces
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < cols * kWavesPerBlock; i += kBlock) {
+      const uint32_t r = i / kWavesPerBlock, ww = i % kWavesPerBlock;
+      hist[(size_t)r * n_slices + b * kWavesPerBlock + ww] = lds[ww * cols + r];
+    }
+  }
+}
+
+// Exclusive scan over the workgroup of one value per thread; returns the total.
+// tmp: one LDS word per wave.
+template <int WAVES>
+__device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t &excl, uint32_t *tmp) {
   const uint32_t lane = lane_id(), w = threadIdx.x / kWave;
   uint32_t incl = v;
 #pragma unroll
   for (int s = 1; s < kWave; s <<= 1) {
-    uint32_t o = __shfl_up(incl, s, kWave);
+    const uint32_t o = __shfl_up(incl, s, kWave);
     if (lane >= (uint32_t)s) incl += o;
   }
-  if (lane == kWave - 1) lds_tmp[w] = incl;
+  if (lane == kWave - 1) tmp[w] = incl;
   __syncthreads();
   uint32_t base = 0, total = 0;
-  for (int k = 0; k < kWavesPerBlock; ++k) {
-    uint32_t t = lds_tmp[k];
-    if (k < (int)w) base += t;
+#pragma unroll
+  for (int k = 0; k < WAVES; ++k) {
+    const uint32_t t = tmp[k];
+    base += k < (int)w ? t : 0u;
     total += t;
   }
   __syncthreads();
@@ -166,28 +191,28 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t &excl, uint32_t *l
   return total;
 }
 
-__global__ void __launch_bounds__(kBlock)
+// Workgroup d scans row d of hist[cols][n_slices]; thread i owns slices
+// [i * kScanPerThread, ...) and loads all of them at once.
+__global__ void __launch_bounds__(kScanThreads)
 bins_scan(uint32_t *__restrict__ hist, uint32_t n_slices, uint32_t n_decoders,
           uint32_t *__restrict__ bin_count, uint32_t *__restrict__ status,
           uint32_t *__restrict__ invalid_out) {
-  __shared__ uint32_t lds_tmp[kWavesPerBlock];
-  const uint32_t d = blockIdx.x;  // row; row n_decoders counts invalid queries
+  __shared__ uint32_t tmp[kScanThreads / kWave];
+  const uint32_t d = blockIdx.x;
+  const uint32_t s0 = threadIdx.x * kScanPerThread;
   uint32_t *row = hist + (size_t)d * n_slices;
-  // each thread owns kScanPerThread consecutive slices of the row (n_slices is
-  // at most kBlock * kScanPerThread); all of them are loaded at once
-  const uint32_t lo = threadIdx.x * kScanPerThread;
   uint32_t v[kScanPerThread];
   uint32_t sum = 0;
 #pragma unroll
   for (int k = 0; k < kScanPerThread; ++k) {
-    v[k] = lo + k < n_slices ? row[lo + k] : 0u;
+    v[k] = s0 + k < n_slices ? row[s0 + k] : 0u;
     sum += v[k];
   }
   uint32_t excl;
-  const uint32_t total = block_exclusive_scan(sum, excl, lds_tmp);
+  const uint32_t total = block_exclusive_scan<kScanThreads / kWave>(sum, excl, tmp);
 #pragma unroll
   for (int k = 0; k < kScanPerThread; ++k) {
-    if (lo + k < n_slices) row[lo + k] = excl;
+    if (s0 + k < n_slices) row[s0 + k] = excl;
     excl += v[k];
   }
   if (threadIdx.x == 0) {
@@ -200,86 +225,61 @@ bins_scan(uint32_t *__restrict__ hist, uint32_t n_slices, uint32_t n_decoders,
   }
 }
 
+template <bool REG>
 __global__ void __launch_bounds__(kBlock)
-bins_scatter(const uint16_t *__restrict__ dec16, uint32_t n, uint32_t n_decoders,
-             uint32_t align, uint32_t chunk, uint32_t n_slices,
-             const uint32_t *__restrict__ hist, const uint32_t *__restrict__ bin_count,
-             uint32_t *__restrict__ bin_offset, uint32_t *__restrict__ perm) {
+bins_place(const uint32_t *__restrict__ tex_id, uint32_t n,
+           const uint32_t *__restrict__ tex_to_dec, uint32_t n_textures, uint32_t n_decoders,
+           uint32_t align, uint32_t chunk, const uint32_t *__restrict__ hist,
+           const uint32_t *__restrict__ bin_count, uint32_t *__restrict__ bin_offset,
+           uint32_t *__restrict__ perm) {
   extern __shared__ uint32_t lds[];  // kWavesPerBlock x n_decoders cursors
-  __shared__ uint32_t lds_tmp[kWavesPerBlock];
-  const uint32_t b = blockIdx.x, w = threadIdx.x / kWave, lane = lane_id();
-  const uint32_t nblocks = gridDim.x;
+  __shared__ uint32_t scan_tmp[kWavesPerBlock];
+  const uint32_t D = n_decoders;
+  const uint32_t b = xcd_local_block(blockIdx.x, gridDim.x), lane = lane_id();
+  const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const uint32_t nblocks = gridDim.x, n_slices = nblocks * kWavesPerBlock;
   const Slice sl = slice_of(b, w, chunk, n);
-  // Lanes past the slice read as invalid.  The first batch is in flight
-  // during the offset scan below.
-  auto fetch = [&](uint64_t base, uint32_t (&v)[kRowsPerBatch]) {
-#pragma unroll
-    for (int j = 0; j < kRowsPerBatch; ++j) {
-      const uint64_t q = base + (uint64_t)j * kWave + lane;
-      v[j] = q < sl.end ? dec16[q] : kInvalid16;
-    }
-  };
-  uint32_t nxt[kRowsPerBatch];
-  if (sl.beg < sl.end) fetch(sl.beg, nxt);
+  // The first batch's ids are in flight during the offset scan below; invalid
+  // queries are marked as outside: they go nowhere.
+  uint32_t d[kBatchRows];
+  if (sl.beg < sl.end)
+    load_batch(tex_id, tex_to_dec, n_textures, D, kOutside, sl.beg, sl.end, lane, d);
   // Padded bin offsets: thread i owns decoders [dlo, dhi).
-  const uint32_t dper = (n_decoders + kBlock - 1) / kBlock;
-  const uint32_t dlo = min(threadIdx.x * dper, n_decoders);
-  const uint32_t dhi = min(dlo + dper, n_decoders);
+  const uint32_t dper = (D + kBlock - 1) / kBlock;
+  const uint32_t dlo = min(threadIdx.x * dper, D);
+  const uint32_t dhi = min(dlo + dper, D);
   uint32_t psum = 0;
   for (uint32_t k = dlo; k < dhi; ++k) psum += (bin_count[k] + align - 1) & ~(align - 1);
   uint32_t off;
-  const uint32_t total = block_exclusive_scan(psum, off, lds_tmp);
+  const uint32_t total = block_exclusive_scan<kWavesPerBlock>(psum, off, scan_tmp);
+  // the slices' prefixes of decoder k: one 16-byte piece (n_slices is a
+  // multiple of 4 and hist 16-byte aligned)
+  static_assert(kWavesPerBlock == 4, "one 16-byte piece per decoder");
+  const uint32_t *prefix = hist + b * kWavesPerBlock;
   for (uint32_t k = dlo; k < dhi; ++k) {
-    const uint32_t c = bin_count[k];
-    const uint32_t padded = (c + align - 1) & ~(align - 1);
-#pragma unroll
-    for (int i = 0; i < kWavesPerBlock; ++i)
-      lds[i * n_decoders + k] = off + hist[(size_t)k * n_slices + b * kWavesPerBlock + i];
+    const uint32_t cnt = bin_count[k];
+    const uint32_t padded = (cnt + align - 1) & ~(align - 1);
+    const uint4 p = *(const uint4 *)(prefix + (size_t)k * n_slices);
+    lds[0 * D + k] = off + p.x;
+    lds[1 * D + k] = off + p.y;
+    lds[2 * D + k] = off + p.z;
+    lds[3 * D + k] = off + p.w;
     if (b == 0) bin_offset[k] = off;
     if (k % nblocks == b)  // the padding slots of bin k
-      for (uint32_t s = off + c; s < off + padded; ++s) perm[s] = NTC_PAD;
+      for (uint32_t s = off + cnt; s < off + padded; ++s) perm[s] = NTC_PAD;
     off += padded;
   }
-  if (b == 0 && threadIdx.x == 0) bin_offset[n_decoders] = total;
+  if (b == 0 && threadIdx.x == 0) bin_offset[D] = total;
   __syncthreads();
-  uint32_t *cur = lds + w * n_decoders;
-  // (cd, cc): a decoder whose cursor lives in a register while whole rows of
-  // it follow one another; cur[cd] is stale meanwhile.
-  uint32_t cd = kOutside, cc = 0;
+  WaveTable<REG> cur{0u, lds + w * D};
+  if constexpr (REG) cur.reg = lane < D ? cur.lds[lane] : 0u;
   for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
-    uint32_t v[kRowsPerBatch];
+    if (base != sl.beg)
+      load_batch(tex_id, tex_to_dec, n_textures, D, kOutside, base, sl.end, lane, d);
 #pragma unroll
-    for (int j = 0; j < kRowsPerBatch; ++j) v[j] = nxt[j];
-    if (base + kWaveQuantum < sl.end) fetch(base + kWaveQuantum, nxt);
-#pragma unroll
-    for (int j = 0; j < kRowsPerBatch; ++j) {
-      const uint32_t q = (uint32_t)(base + (uint64_t)j * kWave + lane);
-      const uint32_t d = v[j] == kInvalid16 ? n_decoders : v[j];  // lanes past the end: invalid
-      const uint32_t v0 = __builtin_amdgcn_readfirstlane(d);
-      if (ballot(d == v0) == ~0ull && v0 < n_decoders) {
-        if (v0 != cd) {
-          if (cd != kOutside && lane == 0) cur[cd] = cc;
-          cd = v0;
-          cc = cur[v0];
-        }
-        perm[cc + lane] = q;
-        cc += kWave;
-      } else {
-        if (cd != kOutside) {
-          if (lane == 0) cur[cd] = cc;
-          cd = kOutside;
-        }
-        uint64_t todo = ballot(d < n_decoders);
-        while (todo) {
-          const uint32_t leader = (uint32_t)__builtin_ctzll(todo);
-          const uint32_t dl = read_lane(d, leader);
-          const uint64_t same = ballot(d == dl) & todo;
-          const uint32_t at = cur[dl];  // same address in every lane
-          if (d == dl) perm[at + lanes_below(same)] = q;
-          if (lane == leader) cur[dl] = at + (uint32_t)__builtin_popcountll(same);
-          todo &= ~same;
-        }
-      }
+    for (int j = 0; j < kBatchRows; ++j) {
+      const uint32_t pos = rank_row<REG, true>(d[j], cur, lane);
+      if (d[j] != kOutside) perm[pos] = (uint32_t)(base + (uint64_t)j * kWave + lane);
     }
   }
 }
@@ -297,19 +297,18 @@ int allow_lds(const void *kernel, size_t bytes) {
 
 BinsLayout bins_layout(int64_t n, int32_t n_decoders) {
   BinsLayout L;
-  int64_t chunk = (n + kTargetBlocks - 1) / kTargetBlocks;
+  // fewer, longer slices for many decoders: the histograms stay within 4 MiB
+  int64_t max_blocks = kMaxHistWords / ((int64_t)kWavesPerBlock * (n_decoders + 1));
+  max_blocks = max_blocks < 1 ? 1 : max_blocks > kTargetBlocks ? kTargetBlocks : max_blocks;
+  int64_t chunk = (n + max_blocks - 1) / max_blocks;
   chunk = (chunk + kChunkQuantum - 1) / kChunkQuantum * kChunkQuantum;
-  if (chunk < kMinChunk) chunk = kMinChunk;
+  if (chunk < kChunkQuantum) chunk = kChunkQuantum;
   L.chunk = chunk;
   L.blocks = n > 0 ? (n + chunk - 1) / chunk : 1;
   L.hist_words = (size_t)(n_decoders + 1) * (size_t)L.blocks * kWavesPerBlock;
-  L.dec_offset = ((kStatusWords + L.hist_words) * sizeof(uint32_t) + 15) & ~(size_t)15;
-  L.bytes = L.dec_offset + (((size_t)n * sizeof(uint16_t) + 15) & ~(size_t)15);
+  L.bytes = (kStatusWords + L.hist_words) * sizeof(uint32_t);
   return L;
 }
-
-static_assert(kTargetBlocks * kWavesPerBlock <= (int64_t)kBlock * kScanPerThread,
-              "the row scan covers every slice");
 
 int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
                       int32_t n_textures, int32_t n_decoders, int32_t align,
@@ -318,22 +317,33 @@ int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_
   const BinsLayout L = bins_layout(n, n_decoders);
   uint32_t *status = (uint32_t *)workspace;
   uint32_t *hist = status + kStatusWords;
-  uint16_t *dec16 = (uint16_t *)((char *)workspace + L.dec_offset);
   const uint32_t D = (uint32_t)n_decoders;
   const uint32_t n_slices = (uint32_t)L.blocks * kWavesPerBlock;
-  const size_t lds_hist = (size_t)kWavesPerBlock * (D + 1) * sizeof(uint32_t);
-  const size_t lds_scatter = (size_t)kWavesPerBlock * D * sizeof(uint32_t);
-  int st = allow_lds((const void *)bins_hist, lds_hist);
-  if (st == NTC_OK) st = allow_lds((const void *)bins_scatter, lds_scatter);
+  const bool reg = D <= kRegDecoders;
+  const size_t lds_count = reg ? 0 : (size_t)kWavesPerBlock * (D + 1) * sizeof(uint32_t);
+  const size_t lds_place = (size_t)kWavesPerBlock * D * sizeof(uint32_t);
+  const void *count_fn = reg ? (const void *)bins_count<true> : (const void *)bins_count<false>;
+  const void *place_fn = reg ? (const void *)bins_place<true> : (const void *)bins_place<false>;
+  int st = allow_lds(count_fn, lds_count);
+  if (st == NTC_OK) st = allow_lds(place_fn, lds_place);
   if (st != NTC_OK) return st;
-  hipLaunchKernelGGL(bins_hist, dim3((unsigned)L.blocks), dim3(kBlock), lds_hist, stream, tex_id,
-                     (uint32_t)n, tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, n_slices,
-                     hist, dec16);
-  hipLaunchKernelGGL(bins_scan, dim3(D + 1), dim3(kBlock), 0, stream, hist, n_slices, D,
+  const dim3 grid((unsigned)L.blocks), block(kBlock);
+  if (reg)
+    hipLaunchKernelGGL(bins_count<true>, grid, block, lds_count, stream, tex_id, (uint32_t)n,
+                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist);
+  else
+    hipLaunchKernelGGL(bins_count<false>, grid, block, lds_count, stream, tex_id, (uint32_t)n,
+                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist);
+  hipLaunchKernelGGL(bins_scan, dim3(D + 1), dim3(kScanThreads), 0, stream, hist, n_slices, D,
                      bin_count, status, invalid_out);
-  hipLaunchKernelGGL(bins_scatter, dim3((unsigned)L.blocks), dim3(kBlock), lds_scatter, stream,
-                     dec16, (uint32_t)n, D, (uint32_t)align, (uint32_t)L.chunk, n_slices, hist,
-                     bin_count, bin_offset, perm);
+  if (reg)
+    hipLaunchKernelGGL(bins_place<true>, grid, block, lds_place, stream, tex_id, (uint32_t)n,
+                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk,
+                       hist, bin_count, bin_offset, perm);
+  else
+    hipLaunchKernelGGL(bins_place<false>, grid, block, lds_place, stream, tex_id, (uint32_t)n,
+                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk,
+                       hist, bin_count, bin_offset, perm);
   return hip_status(hipGetLastError());
 }
 

@@ -48,7 +48,6 @@ struct BinsLayout {
   int64_t chunk;      // queries per workgroup
   int64_t blocks;     // workgroups of the histogram / scatter kernels
   size_t hist_words;  // (n_decoders + 1) * blocks
-  size_t dec_offset;  // byte offset of the 16-bit decoder ids (16-byte aligned)
   size_t bytes;       // total workspace bytes
 };
 

@@ -168,7 +168,7 @@ def build_bins(tex_id: torch.Tensor, tex_to_dec: torch.Tensor, n_decoders: int, 
     return bins
 
 
-NOALLOC_SCRATCH_BYTES = 64 << 20  # NTC_NOALLOC_SCRATCH_BYTES
+NOALLOC_SCRATCH_BYTES = 5 << 20  # NTC_NOALLOC_SCRATCH_BYTES
 
 
 def build_bins_noalloc(tex_id: torch.Tensor, tex_to_dec: torch.Tensor, n_decoders: int,

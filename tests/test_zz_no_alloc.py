@@ -58,16 +58,21 @@ def test_noalloc_matches_workspace_path(sizes):
             assert int(inv.item()) > 0
 
 
-def test_noalloc_rejects_a_call_past_its_scratch():
+def test_noalloc_largest_sizes_fit():
+    """The scratch holds the workspace of every valid call: 40M queries with the
+    largest decoder count, then a small call, both equal to ntc_build_bins."""
     dev = torch.device("cuda:0")
-    n, D = 40_000_000, 2
-    tex = torch.zeros(n, dtype=torch.int32, device=dev)
-    t2d = torch.zeros(4, dtype=torch.int32, device=dev)
-    cnt = torch.zeros(D, dtype=torch.int32, device=dev)
-    off = torch.zeros(D + 1, dtype=torch.int32, device=dev)
-    perm = torch.zeros(ntc.perm_capacity(n, D), dtype=torch.int32, device=dev)
-    with pytest.raises(ntc.NtcError) as e:
-        ntc.build_bins_noalloc(tex, t2d, D, cnt, off, perm)
-    assert e.value.status == ntc.NTC_ERR_CAPACITY
-    torch.cuda.synchronize()
-    assert int(off.abs().sum().item()) == 0  # nothing was enqueued
+    for k, (n, T, D, align) in enumerate(((40_000_000, 4096, 4096, 64), (1000, 3, 4096, 1))):
+        tex, t2d = _inputs(300 + k, n, T, D, 0)
+        tex_d = torch.from_numpy(tex.view(np.int32)).to(dev)
+        t2d_d = torch.from_numpy(t2d.view(np.int32)).to(dev)
+        assert ntc.workspace_bytes(n, D) <= ntc.NOALLOC_SCRATCH_BYTES
+        ref = ntc.build_bins(tex_d, t2d_d, D, align)
+        cnt, off, perm, inv = _noalloc(tex_d, t2d_d, D, align, dev)
+        torch.cuda.synchronize()
+        assert torch.equal(cnt, ref.bin_count) and torch.equal(off, ref.bin_offset)
+        P = int(ref.bin_offset[-1].item())
+        assert torch.equal(perm[:P], ref.perm[:P])
+        assert int(inv.item()) == 0
+        del tex_d, ref, perm
+        torch.cuda.empty_cache()
