@@ -4,7 +4,8 @@ widths, invalid ids and texture layouts; the decode over random combinations
 of every supported decoder shape and variant (levels x channels, hidden width,
 depth, output width, mip blending, LeakyReLU, fp16 rows, small and odd level
 resolutions, uv far outside [0, 1)), with the LDS-staged gather where it
-applies.  Bins and divergence must be bit-exact, decoded channels within 2e-3,
+applies; the 2-D divergence map over random screens, samples per pixel, block
+shapes, decoder counts and invalid ids.  Bins and divergence must be bit-exact, decoded channels within 2e-3,
 stream and binned order bit-identical."""
 import sys
 
@@ -132,3 +133,69 @@ def test_random_decode(dev, oracle, seed):
         err_g = np.abs(out_g.cpu().numpy().astype(np.float64) - ref).max()
         say(f"    staged gather max abs err {err_g:.3e}")
         assert err_g <= TOL
+
+
+def _map_case(rng, seed):
+    """Random screen, samples per pixel, block shape (both kernel paths: power-of-two
+    row segments up to 64 samples and at most 16 rows, and any other shape), texture
+    layout, decoder count (bitmaps of several words) and invalid ids."""
+    spp = int(rng.choice([1, 1, 2, 3, 4, 8]))
+    W_ = int(rng.integers(1, 300))
+    H_ = int(rng.integers(1, 200))
+    if rng.random() < 0.5:  # a tiled shape: block_w * spp a power of two <= 64
+        g = int(rng.choice([g for g in (1, 2, 4, 8, 16, 32, 64) if g % spp == 0] or [spp]))
+        bw, bh = max(1, g // spp), int(rng.integers(1, 17))
+    else:
+        bw, bh = int(rng.integers(1, 40)), int(rng.integers(1, 40))
+    T = int(rng.integers(1, 200))
+    D = int(rng.choice([int(rng.integers(1, 30)), int(rng.integers(33, 300))]))
+    bad = seed % 2 == 0
+    t2d = rng.integers(0, D + (2 if bad else 0), T).astype(np.uint32)
+    tex = texture_stream(rng, W_ * H_ * spp, T + (3 if bad else 0))
+    hist_len = int(rng.integers(1, 20))
+    return W_, H_, spp, bw, bh, T, D, t2d, tex, hist_len
+
+
+def _check_map(dev, oracle, W_, H_, spp, bw, bh, T, D, t2d, tex, hist_len):
+    tex_d = torch.from_numpy(tex.view(np.int32)).to(dev)
+    t2d_d = torch.from_numpy(t2d.view(np.int32)).to(dev)
+    dmap, hist, tot = ntc.divergence_map(tex_d, W_, H_, t2d_d, D, spp=spp, block_w=bw,
+                                         block_h=bh, hist_len=hist_len, n_textures=T)
+    dmap_o, hist_o, tot_o = oracle.divergence_map(tex, W_, H_, t2d, D, spp=spp, block_w=bw,
+                                                  block_h=bh, hist_len=hist_len, n_textures=T)
+    assert np.array_equal(u32(dmap), dmap_o)
+    assert np.array_equal(u32(hist), hist_o)
+    assert np.array_equal(tot.cpu().numpy().astype(np.uint64), tot_o)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_divergence_map(dev, oracle, seed):
+    rng = np.random.default_rng(9000 + seed)
+    case = _map_case(rng, seed)
+    W_, H_, spp, bw, bh, T, D = case[:7]
+    say(f"[random map] seed={seed} {W_}x{H_}x{spp} block {bw}x{bh} T={T} D={D} "
+        f"blocks={((W_ + bw - 1) // bw) * ((H_ + bh - 1) // bh)} hist_len={case[-1]}")
+    _check_map(dev, oracle, *case)
+
+
+def test_divergence_map_one_block_of_2_20_samples(dev, oracle):
+    """One block of 1024 x 1024 samples (the integer-division branch of the sample
+    walk) with ids over many bitmap words, beside a second, partial block."""
+    rng = np.random.default_rng(77)
+    W_, H_, spp, T, D = 1500, 1024, 1, 700, 600
+    t2d = rng.integers(0, D + 1, T).astype(np.uint32)
+    tex = texture_stream(rng, W_ * H_ * spp, T + 2)
+    say("[map] 2^20-sample block")
+    _check_map(dev, oracle, W_, H_, spp, 1024, 1024, T, D, t2d, tex, 40)
+
+
+@pytest.mark.parametrize("W_,H_,spp,bw,bh", [(3840, 2160, 1, 8, 8), (1920, 1080, 4, 16, 16),
+                                            (999, 777, 2, 32, 1), (1000, 1000, 1, 64, 16)])
+def test_divergence_map_large_frames(dev, oracle, W_, H_, spp, bw, bh):
+    """Frame-sized maps, block counts that are not multiples of 16 waves."""
+    rng = np.random.default_rng(W_ + H_)
+    T, D = 512, 16
+    t2d = rng.integers(0, D, T).astype(np.uint32)
+    tex = texture_stream(rng, W_ * H_ * spp, T)
+    say(f"[map] {W_}x{H_}x{spp} block {bw}x{bh}")
+    _check_map(dev, oracle, W_, H_, spp, bw, bh, T, D, t2d, tex, 17)
