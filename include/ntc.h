@@ -236,13 +236,21 @@ typedef struct {
  *   NTC_ENGINE_FMA: every lane evaluates its own query's decoder with vector
  *     fp16 dot products (fp32 accumulation), reading that decoder's weights
  *     itself, so a wave's cost does not depend on how many decoders it holds
- *     (the paper's Non-Shared FMA).  Stream mode only (NTC_ERR_UNSUPPORTED with
- *     bin_offset); dims[n_layers] must be 8 or 16 (NTC_ERR_UNSUPPORTED) and
- *     decoders->params 16-byte aligned (NTC_ERR_ARG).  Results agree with the
- *     MFMA engine within rounding, not bit for bit.
+ *     (the paper's Non-Shared FMA).  With hidden width 64 the weights come from
+ *     a per-CU LDS cache of whole decoders (a tile of 1024 queries stages the
+ *     decoders it misses; a tile with more distinct decoders than the cache
+ *     holds takes several passes); other widths read them as with
+ *     NTC_ENGINE_FMA_DIRECT.
+ *   NTC_ENGINE_FMA_DIRECT: the same per-lane evaluation with every lane
+ *     loading its weight rows through the L1/L2 caches (16-byte loads).
+ *   Both FMA engines: stream mode only (NTC_ERR_UNSUPPORTED with bin_offset);
+ *     dims[n_layers] must be 8 or 16 (NTC_ERR_UNSUPPORTED) and decoders->params
+ *     16-byte aligned (NTC_ERR_ARG).  Results agree with the MFMA engine within
+ *     rounding, not bit for bit, and with each other bit for bit.
  */
 #define NTC_ENGINE_MFMA 0
 #define NTC_ENGINE_FMA 1
+#define NTC_ENGINE_FMA_DIRECT 2
 
 /*
  * Latent gathers (Sec. 1: each query samples its texture's latent grid):

@@ -139,9 +139,11 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
     return NTC_ERR_ARG;
   if (o.output_format != NTC_OUT_F32 && o.output_format != NTC_OUT_F16) return NTC_ERR_ARG;
   if (o.pe_octaves != 0 && o.pe_octaves != 4 && o.pe_octaves != 8) return NTC_ERR_ARG;
-  if (o.engine != NTC_ENGINE_MFMA && o.engine != NTC_ENGINE_FMA) return NTC_ERR_ARG;
+  if (o.engine != NTC_ENGINE_MFMA && o.engine != NTC_ENGINE_FMA &&
+      o.engine != NTC_ENGINE_FMA_DIRECT)
+    return NTC_ERR_ARG;
   if (o.gather != NTC_GATHER_DIRECT && o.gather != NTC_GATHER_STAGED) return NTC_ERR_ARG;
-  const bool fma = o.engine == NTC_ENGINE_FMA;
+  const bool fma = o.engine != NTC_ENGINE_MFMA;
   const int64_t elem = o.output_format == NTC_OUT_F16 ? 2 : 4;
   if (q->n < 0 || q->n > kMaxQueries) return NTC_ERR_ARG;
   if (g->n_textures < 1 || g->n_levels < 1 || g->n_levels > NTC_MAX_LEVELS) return NTC_ERR_ARG;
@@ -222,6 +224,7 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
   a.out_f16 = o.output_format == NTC_OUT_F16;
   a.pe_octaves = o.pe_octaves;
   a.gather = o.gather;
+  a.fma_cache = o.engine == NTC_ENGINE_FMA;
   if (o.gather == NTC_GATHER_STAGED &&
       (fma || !binned || q->mip || L != 2 || out_dim > 8))
     return NTC_ERR_UNSUPPORTED;

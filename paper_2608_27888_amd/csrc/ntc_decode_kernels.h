@@ -1270,13 +1270,239 @@ int launch_fma(const DecodeArgs &a, hipStream_t stream) {
   return hip_status(hipGetLastError());
 }
 
+// ------------------------------------- non-shared FMA decode, LDS weight cache
+//
+// The same per-lane computation with the weights read from LDS: one workgroup
+// of kFmaLdsThreads threads per CU walks tiles of that many consecutive
+// queries and keeps up to `slots` whole decoders in an LDS cache.  For each
+// tile it looks up every query's decoder, stages the missing ones into slots
+// no pending query of the tile uses (one cooperative copy), and every lane
+// whose decoder is cached evaluates its own query with v_dot2c_f32_f16 on rows
+// read from its decoder's slot; a tile with more distinct decoders than slots
+// takes several passes.  Lanes of one wave that use different decoders read
+// different slots in one instruction.  Hidden width 64: activations stay in
+// registers (the row loops are unrolled).
+constexpr int kFmaLdsThreads = 1024;
+constexpr int kFmaLdsWaves = kFmaLdsThreads / kWave;
+constexpr size_t kFmaLdsWeightBytes = 144 * 1024;  // the decoder cache
+constexpr uint32_t kFmaMaxSlots = 16;
+constexpr uint32_t kNoSlotDecoder = 0xFFFFFFFFu;
+
+struct FmaCache {
+  uint32_t slot_dec[kFmaMaxSlots];  // decoder held by each slot
+  uint32_t used[kFmaMaxSlots];      // a pending query of this pass hit the slot
+  uint32_t want[kFmaLdsWaves][kFmaMaxSlots];  // per wave: distinct missing decoders
+  uint32_t n_want[kFmaLdsWaves];
+  uint32_t stage_slot[kFmaMaxSlots], stage_dec[kFmaMaxSlots];
+  uint32_t n_stage;
+};
+
+// Layer DIN -> 64 (activated, fp16 pairs) from a decoder's weights in LDS.
+template <int DIN>
+__device__ __forceinline__ void fma_hidden_lds(const uint16_t *W, const uint32_t (&h)[DIN / 2],
+                                               uint32_t (&o)[32], bool leaky, uint32_t slope_h2) {
+  const uint16_t *b = W + 64 * DIN;
+#pragma unroll
+  for (int j = 0; j < 64; j += 2) {
+    const float2 bj = unpack_half2(*(const uint32_t *)(b + j));
+    float acc0 = bj.x, acc1 = bj.y;
+    const u32x4 *r0 = (const u32x4 *)(W + j * DIN);
+    const u32x4 *r1 = (const u32x4 *)(W + (j + 1) * DIN);
+#pragma unroll
+    for (int k = 0; k < DIN / 8; ++k) {
+      const u32x4 w0 = r0[k], w1 = r1[k];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc0 = dot2(w0[e], h[4 * k + e], acc0);
+        acc1 = dot2(w1[e], h[4 * k + e], acc1);
+      }
+    }
+    o[j / 2] = leaky ? leaky_pack2(acc0, acc1, slope_h2) : relu_pack2(acc0, acc1);
+  }
+}
+
+// Output layer 64 -> dout (8 or 16), logistic sigmoid, from LDS.
+__device__ __forceinline__ void fma_out_lds(const uint16_t *W, int dout, const uint32_t (&h)[32],
+                                            float (&y)[16]) {
+  const uint16_t *b = W + dout * 64;
+#pragma unroll
+  for (int j = 0; j < 16; j += 2) {
+    if (j < dout) {
+      const float2 bj = unpack_half2(*(const uint32_t *)(b + j));
+      float acc0 = bj.x, acc1 = bj.y;
+      const u32x4 *r0 = (const u32x4 *)(W + j * 64);
+      const u32x4 *r1 = (const u32x4 *)(W + (j + 1) * 64);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const u32x4 w0 = r0[k], w1 = r1[k];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc0 = dot2(w0[e], h[4 * k + e], acc0);
+          acc1 = dot2(w1[e], h[4 * k + e], acc1);
+        }
+      }
+      y[j] = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(acc0 * -kLog2e));
+      y[j + 1] = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(acc1 * -kLog2e));
+    } else {
+      y[j] = y[j + 1] = 0.f;
+    }
+  }
+}
+
+template <int NL, int CH, int PE, bool MIP>
+__global__ void __launch_bounds__(kFmaLdsThreads)
+decode_fma_lds(const DecodeArgs a, uint32_t slots, uint32_t n_tiles) {
+  using S = Shape<NL, CH, PE, 64>;
+  extern __shared__ __attribute__((aligned(16))) uint16_t wcache[];
+  __shared__ FmaCache c;
+  const uint32_t tid = threadIdx.x, lane = lane_id();
+  const uint32_t w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const uint32_t stride = (uint32_t)a.dec_stride;  // halves, a multiple of 8
+  const uint32_t D = (uint32_t)a.n_decoders;
+  const bool leaky = a.leaky != 0;
+  if (tid < kFmaMaxSlots) {
+    c.slot_dec[tid] = kNoSlotDecoder;
+    c.used[tid] = 0;
+  }
+  for (uint32_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    const uint64_t q64 = (uint64_t)tile * kFmaLdsThreads + tid;
+    const uint32_t q = (uint32_t)q64;
+    const Query qq = validate(a, load_query<NL, MIP>(a, q, q64 < a.n));
+    uint32_t d = qq.valid ? a.tex_to_dec[qq.tex] : kNoSlotDecoder;
+    if (d >= D) d = kNoSlotDecoder;
+    bool pending = d != kNoSlotDecoder;
+    uint32_t x[S::F / 2];
+    gather<NL, CH, PE, MIP>(a, qq, x);  // an invalid query gathers texture 0, unused
+    while (__syncthreads_or(pending)) {
+      // look the decoder up; mark the slots this pass reads; list the misses
+      int slot = -1;
+      if (pending)
+        for (uint32_t k = 0; k < slots; ++k)
+          if (c.slot_dec[k] == d) slot = (int)k;
+      if (pending && slot >= 0) c.used[slot] = 1;
+      const bool miss = pending && slot < 0;
+      uint64_t todo = ballot(miss);
+      uint32_t nw = 0;
+      while (todo) {
+        const uint32_t dl = read_lane(d, (uint32_t)__builtin_ctzll(todo));
+        todo &= ~ballot(d == dl);
+        if (lane == 0 && nw < kFmaMaxSlots) c.want[w][nw] = dl;
+        ++nw;
+      }
+      if (lane == 0) c.n_want[w] = nw < kFmaMaxSlots ? nw : kFmaMaxSlots;
+      __syncthreads();
+      // one thread plans: distinct wanted decoders into slots no pending query hit
+      if (tid == 0) {
+        uint32_t ns = 0, next = 0;
+        bool full = false;
+        for (int wv = 0; wv < kFmaLdsWaves && !full; ++wv)
+          for (uint32_t i = 0; i < c.n_want[wv] && !full; ++i) {
+            const uint32_t dl = c.want[wv][i];
+            bool dup = false;
+            for (uint32_t k = 0; k < ns; ++k) dup = dup || c.stage_dec[k] == dl;
+            if (dup) continue;
+            while (next < slots && c.used[next]) ++next;
+            if (next == slots) {
+              full = true;
+              break;
+            }
+            c.stage_slot[ns] = next;
+            c.stage_dec[ns] = dl;
+            ++ns;
+            ++next;
+          }
+        c.n_stage = ns;
+        for (uint32_t k = 0; k < ns; ++k) c.slot_dec[c.stage_slot[k]] = c.stage_dec[k];
+        for (uint32_t k = 0; k < slots; ++k) c.used[k] = 0;
+      }
+      __syncthreads();
+      // every thread copies 16-byte pieces of the staged decoders
+      const uint32_t ns = c.n_stage;
+      for (uint32_t k = 0; k < ns; ++k) {
+        const u32x4 *src = (const u32x4 *)(a.params + (size_t)c.stage_dec[k] * stride);
+        u32x4 *dst = (u32x4 *)(wcache + (size_t)c.stage_slot[k] * stride);
+        for (uint32_t i = tid; i < stride / 8; i += kFmaLdsThreads) dst[i] = src[i];
+      }
+      __syncthreads();
+      if (pending && slot < 0)
+        for (uint32_t k = 0; k < slots; ++k)
+          if (c.slot_dec[k] == d) slot = (int)k;
+      if (pending && slot >= 0) {
+        pending = false;
+        const uint16_t *p = wcache + (size_t)slot * stride;
+        uint32_t h[32], o[32];
+        fma_hidden_lds<S::F>(p, x, h, leaky, a.slope_h2);
+        p += 64 * (S::F + 1);
+        for (int l = 0; l < a.n_hidden; ++l) {
+          fma_hidden_lds<64>(p, h, o, leaky, a.slope_h2);
+#pragma unroll
+          for (int i = 0; i < 32; ++i) h[i] = o[i];
+          p += 64 * 65;
+        }
+        float y[16];
+        fma_out_lds(p, a.out_dim, h, y);
+        const int out_dim = a.out_dim;
+        if (a.out_f16) {
+          u32x2 *o2 = (u32x2 *)((uint16_t *)a.out + (size_t)q * out_dim);
+#pragma unroll
+          for (int cc = 0; cc < 16; cc += 4)
+            if (cc < out_dim)
+              o2[cc / 4] = u32x2{pack_half2(y[cc], y[cc + 1]), pack_half2(y[cc + 2], y[cc + 3])};
+        } else {
+          floatx4 *o4 = (floatx4 *)((float *)a.out + (size_t)q * out_dim);
+#pragma unroll
+          for (int cc = 0; cc < 16; cc += 4)
+            if (cc < out_dim) o4[cc / 4] = floatx4{y[cc], y[cc + 1], y[cc + 2], y[cc + 3]};
+        }
+      }
+    }
+  }
+}
+
+// Compute units of the current device (one LDS-cache workgroup each).
+inline int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus < 1)
+    return 256;
+  return cus;
+}
+
+template <int NL, int CH, int PE, bool MIP>
+int launch_fma_lds(const DecodeArgs &a, uint32_t slots, hipStream_t stream) {
+  const void *fn = (const void *)decode_fma_lds<NL, CH, PE, MIP>;
+  const size_t lds = (size_t)slots * (size_t)a.dec_stride * sizeof(uint16_t);
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return NTC_ERR_HIP;
+  const uint64_t n_tiles = ((uint64_t)a.n + kFmaLdsThreads - 1) / kFmaLdsThreads;
+  static const int cus = device_cus();
+  const uint64_t groups = n_tiles < (uint64_t)cus ? n_tiles : (uint64_t)cus;
+  hipLaunchKernelGGL((decode_fma_lds<NL, CH, PE, MIP>), dim3((unsigned)groups),
+                     dim3(kFmaLdsThreads), lds, stream, a, slots, (uint32_t)n_tiles);
+  return hip_status(hipGetLastError());
+}
+
+// Hidden width 64 takes the LDS weight cache when at least one decoder fits it;
+// other shapes read their weights through the caches (decode_fma).
+template <int NL, int CH, int PE, int HID, bool MIP>
+int launch_fma_any(const DecodeArgs &a, hipStream_t stream) {
+  if constexpr (HID == 64) {
+    const size_t bytes = (size_t)a.dec_stride * sizeof(uint16_t);
+    size_t slots = kFmaLdsWeightBytes / bytes;
+    if (slots > kFmaMaxSlots) slots = kFmaMaxSlots;
+    if (slots >= 1 && a.fma_cache) return launch_fma_lds<NL, CH, PE, MIP>(a, (uint32_t)slots, stream);
+  }
+  return launch_fma<NL, CH, PE, HID, MIP>(a, stream);
+}
+
 template <int NL, int CH, int PE, int HID>
 int launch_fma_mip(const DecodeArgs &a, hipStream_t stream) {
   if constexpr (PE > 0) {
-    return a.mip ? NTC_ERR_UNSUPPORTED : launch_fma<NL, CH, PE, HID, false>(a, stream);
+    return a.mip ? NTC_ERR_UNSUPPORTED : launch_fma_any<NL, CH, PE, HID, false>(a, stream);
   } else {
-    return a.mip ? launch_fma<NL, CH, PE, HID, true>(a, stream)
-                 : launch_fma<NL, CH, PE, HID, false>(a, stream);
+    return a.mip ? launch_fma_any<NL, CH, PE, HID, true>(a, stream)
+                 : launch_fma_any<NL, CH, PE, HID, false>(a, stream);
   }
 }
 

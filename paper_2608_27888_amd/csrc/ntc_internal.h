@@ -99,6 +99,7 @@ struct DecodeArgs {
   uint32_t out_f16;                   // output rows: 0 fp32, 1 fp16
   int32_t pe_octaves;                 // positional-encoding octaves (0: none)
   int32_t gather;                     // NTC_GATHER_DIRECT or NTC_GATHER_STAGED
+  int32_t fma_cache;                  // FMA engine: weights through the LDS decoder cache
 };
 
 // Returns NTC_ERR_UNSUPPORTED when no kernel is built for the shape.

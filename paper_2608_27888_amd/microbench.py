@@ -7,7 +7,10 @@ spread uniformly over the lanes, it times
   non_shared : k decoders per wave in stream order, each wave running one MFMA
                MLP pass per decoder present (the paper's Non-Shared WMMA column);
   fma        : the same stream on the per-lane vector-FMA engine, every lane
-               evaluating its own decoder (the paper's Non-Shared FMA column);
+               evaluating its own decoder (the paper's Non-Shared FMA column),
+               its weights read from a per-CU LDS cache of whole decoders;
+  fma_direct : the same engine with every lane loading its weight rows through
+               the L1/L2 caches;
   binned     : the same k-decoder stream binned by decoder id first
                (ntc_build_bins + binned ntc_decode), so each wave runs one pass.
 Times are HIP-event medians of one launch sequence, in microseconds; inputs are
@@ -73,12 +76,16 @@ def main(argv=None):
             def fma():
                 ntc.decode(model, q, None, out=out, engine="fma")
 
+            def fma_direct():
+                ntc.decode(model, q, None, out=out, engine="fma_direct")
+
             row[f"k{k}_stream_us"] = round(median_us(stream, torch), 1)
             row[f"k{k}_binned_us"] = round(median_us(binned, torch), 1)
             row[f"k{k}_fma_us"] = round(median_us(fma, torch), 1)
+            row[f"k{k}_fma_direct_us"] = round(median_us(fma_direct, torch, reps=3, warmup=1), 1)
             print(f"[microbench] side {side} k {k}: stream {row[f'k{k}_stream_us']} us, "
-                  f"binned {row[f'k{k}_binned_us']} us, fma {row[f'k{k}_fma_us']} us",
-                  file=sys.stderr, flush=True)
+                  f"binned {row[f'k{k}_binned_us']} us, fma {row[f'k{k}_fma_us']} us, "
+                  f"fma_direct {row[f'k{k}_fma_direct_us']} us", file=sys.stderr, flush=True)
             del model, q, out, bins
             torch.cuda.empty_cache()
         rows.append(row)
@@ -95,7 +102,10 @@ def main(argv=None):
                 paper_speedup_percent(shared, [r[f"k{k}_fma_us"] for r in rows]), 2),
             "non_shared_fma_vs_binned_percent": round(
                 paper_speedup_percent([r[f"k{k}_binned_us"] for r in rows],
-                                      [r[f"k{k}_fma_us"] for r in rows]), 2)}
+                                      [r[f"k{k}_fma_us"] for r in rows]), 2),
+            "non_shared_mfma_vs_fma_percent": round(
+                paper_speedup_percent([r[f"k{k}_fma_us"] for r in rows],
+                                      [r[f"k{k}_stream_us"] for r in rows]), 2)}
     print(json.dumps({"rows": rows, "summary": summary}), flush=True)
 
 

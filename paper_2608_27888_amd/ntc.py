@@ -271,8 +271,8 @@ def upload(w, device="cuda"):
 
 NTC_ACT_RELU, NTC_ACT_LEAKY_RELU = 0, 1
 NTC_OUT_F32, NTC_OUT_F16 = 0, 1
-NTC_ENGINE_MFMA, NTC_ENGINE_FMA = 0, 1
-ENGINES = {"mfma": NTC_ENGINE_MFMA, "fma": NTC_ENGINE_FMA}
+NTC_ENGINE_MFMA, NTC_ENGINE_FMA, NTC_ENGINE_FMA_DIRECT = 0, 1, 2
+ENGINES = {"mfma": NTC_ENGINE_MFMA, "fma": NTC_ENGINE_FMA, "fma_direct": NTC_ENGINE_FMA_DIRECT}
 NTC_GATHER_DIRECT, NTC_GATHER_STAGED = 0, 1
 GATHERS = {"direct": NTC_GATHER_DIRECT, "staged": NTC_GATHER_STAGED}
 
@@ -290,11 +290,12 @@ def decode(model: DeviceModel, queries: DeviceQueries, bins: Optional[Bins] = No
     """Binned mode when `bins` is given, stream (divergent) mode otherwise.  Hidden
     activation ReLU, or LeakyReLU max(x, slope x) when leaky_slope is given; output
     rows float32 or float16; the model's positional-encoding octaves extend the
-    decoder input.  engine "mfma" (tensor path) or "fma" (per-lane vector FMA,
-    stream mode only); gather "direct" or "staged" (taps staged in LDS, binned
+    decoder input.  engine "mfma" (tensor path), "fma" (per-lane vector FMA with
+    the LDS decoder cache) or "fma_direct" (per-lane vector FMA, weights through
+    the caches); the FMA engines take stream mode only.  gather "direct" or "staged" (taps staged in LDS, binned
     MFMA decode only)."""
     if engine not in ENGINES:
-        raise ValueError("engine must be 'mfma' or 'fma'")
+        raise ValueError("engine must be 'mfma', 'fma' or 'fma_direct'")
     if gather not in GATHERS:
         raise ValueError("gather must be 'direct' or 'staged'")
     if out_dtype not in (torch.float32, torch.float16):

@@ -284,9 +284,10 @@ def test_decode_engine_validation(L):
                                FAKE if binned else None, FAKE if binned else None, cap,
                                64 if binned else 0, ctypes.byref(o), FAKE, None)
 
-    assert call(2) == ntc.NTC_ERR_ARG
+    assert call(3) == ntc.NTC_ERR_ARG
     assert call(-1) == ntc.NTC_ERR_ARG
     assert call(ntc.NTC_ENGINE_FMA, binned=True) == ntc.NTC_ERR_UNSUPPORTED
+    assert call(ntc.NTC_ENGINE_FMA_DIRECT, binned=True) == ntc.NTC_ERR_UNSUPPORTED
     assert call(ntc.NTC_ENGINE_FMA, n=0) == ntc.NTC_OK
     if not HAS_DEVICE:
         assert call(ntc.NTC_ENGINE_FMA) == ntc.NTC_ERR_HIP  # built: launches on FAKE
@@ -297,6 +298,7 @@ def test_decode_engine_validation(L):
     for out_dim in (3, 4, 12):
         d.dims[3] = out_dim
         assert call(ntc.NTC_ENGINE_FMA) == ntc.NTC_ERR_UNSUPPORTED
+        assert call(ntc.NTC_ENGINE_FMA_DIRECT) == ntc.NTC_ERR_UNSUPPORTED
     d.dims[3] = 16
     if not HAS_DEVICE:
         assert call(ntc.NTC_ENGINE_FMA) == ntc.NTC_ERR_HIP

@@ -378,8 +378,9 @@ FMA_CASES = [  # (config, MLP widths or None, LeakyReLU slope or None, output dt
 def test_decode_fma_engine(dev, oracle, name, dims, slope, dtype, pe):
     """The per-lane vector-FMA engine (the paper's Non-Shared FMA, Sec. 4.4)
     against the oracle, in stream order with every decoder mix of the small
-    configurations; it computes the same function as the MFMA engine within
-    rounding."""
+    configurations (tiles with more distinct decoders than the LDS cache holds
+    included); it computes the same function as the MFMA engine within
+    rounding, and the cached and direct weight paths agree bit for bit."""
     w = small(name)
     if pe:
         w = w.with_pe(pe, dims, seed=7)
@@ -388,6 +389,7 @@ def test_decode_fma_engine(dev, oracle, name, dims, slope, dtype, pe):
     say(f"[fma] {name} dims={w.dims} slope={slope} {dtype} pe={pe} n={w.n} D={w.n_decoders}")
     model, q = ntc.upload(w, dev)
     out_f = ntc.decode(model, q, leaky_slope=slope, out_dtype=dtype, engine="fma")
+    out_g = ntc.decode(model, q, leaky_slope=slope, out_dtype=dtype, engine="fma_direct")
     out_m = ntc.decode(model, q, leaky_slope=slope, out_dtype=dtype)
     ref = oracle.decode(w, leaky_slope=slope or 0.0)
     yf = out_f.cpu().numpy().astype(np.float64)
@@ -395,17 +397,20 @@ def test_decode_fma_engine(dev, oracle, name, dims, slope, dtype, pe):
     say(f"    max abs err {err:.3e} (vs MFMA engine {np.abs(yf - out_m.cpu().numpy()).max():.2e})")
     assert err <= TOL
     assert np.all((yf >= 0) & (yf <= 1))
+    iv = torch.int16 if dtype == torch.float16 else torch.int32
+    assert torch.equal(out_f.view(iv), out_g.view(iv))
 
 
-def test_decode_fma_invalid_queries_untouched(dev, oracle):
+@pytest.mark.parametrize("engine", ["fma", "fma_direct"])
+def test_decode_fma_invalid_queries_untouched(dev, oracle, engine):
     w = W.small("tiny")
     w.tex_id = w.tex_id.copy()
     w.tex_id[::13] = 7
     w.tex_to_dec = np.array([0, 1, 0, 9], np.uint32)
-    say("[fma-invalid] tiny with bad ids")
+    say(f"[fma-invalid] tiny with bad ids, {engine}")
     model, q = ntc.upload(w, dev)
     out = torch.full((w.n, w.out_dim), -12345.0, device=dev)
-    ntc.decode(model, q, out=out, engine="fma")
+    ntc.decode(model, q, out=out, engine=engine)
     ref = oracle.decode(w)
     bad = np.isnan(ref[:, 0])
     o = out.cpu().numpy()
@@ -413,14 +418,37 @@ def test_decode_fma_invalid_queries_untouched(dev, oracle):
     assert np.abs(o[~bad] - ref[~bad]).max() <= TOL
 
 
-@pytest.mark.parametrize("n", [1, 63, 65, 255, 257, 4097])
-def test_decode_fma_ragged_sizes(dev, oracle, n):
+@pytest.mark.parametrize("engine", ["fma", "fma_direct"])
+@pytest.mark.parametrize("n", [1, 63, 65, 255, 257, 1023, 1025, 4097])
+def test_decode_fma_ragged_sizes(dev, oracle, n, engine):
     w = W.small("clustered4k")
     w.tex_id, w.uv = w.tex_id[:n].copy(), w.uv[:n].copy()
-    say(f"[fma-ragged] n={n}")
+    say(f"[fma-ragged] n={n} {engine}")
     model, q = ntc.upload(w, dev)
     out = torch.full((n + 7, w.out_dim), -3.0, device=dev)
-    ntc.decode(model, q, out=out[:n], engine="fma")
+    ntc.decode(model, q, out=out[:n], engine=engine)
     o = out.cpu().numpy()
     assert np.abs(o[:n] - oracle.decode(w)).max() <= TOL
     assert np.all(o[n:] == -3.0)  # nothing written past the last row
+
+
+def test_decode_fma_cache_many_decoders_per_tile(dev, oracle):
+    """Every query of a 1024-query tile on its own decoder (far more distinct
+    decoders than the LDS cache holds): each tile takes many passes, and every
+    pass evicts slots of the previous one."""
+    rng = np.random.default_rng(21)
+    T = D = 300
+    res, ch, dims = [16, 8], [16, 16], [32, 64, 64, 8]
+    n = 5000
+    lat = W.draw_latents(21, T, res, ch)
+    params = W.draw_decoders(21, D, dims)
+    t2d = rng.permutation(D).astype(np.uint32)
+    tex = rng.integers(0, T, n).astype(np.uint32)
+    uv = rng.random((n, 2), dtype=np.float32)
+    w = W.Workload("fma_many", T, res, ch, lat, D, dims, params, t2d, tex, uv, None)
+    say("[fma-cache] 300 decoders, random per query")
+    model, q = ntc.upload(w, dev)
+    out_f = ntc.decode(model, q, engine="fma")
+    out_g = ntc.decode(model, q, engine="fma_direct")
+    assert np.abs(out_f.cpu().numpy().astype(np.float64) - oracle.decode(w)).max() <= TOL
+    assert torch.equal(out_f.view(torch.int32), out_g.view(torch.int32))

@@ -128,6 +128,8 @@ def test_random_decode(dev, oracle, seed):
     if w.out_dim % 8 == 0:
         out_f = ntc.decode(model, q, leaky_slope=slope, out_dtype=dtype, engine="fma")
         assert np.abs(out_f.cpu().numpy().astype(np.float64) - ref).max() <= TOL
+        out_g = ntc.decode(model, q, leaky_slope=slope, out_dtype=dtype, engine="fma_direct")
+        assert torch.equal(out_f.view(iv), out_g.view(iv))
     if len(w.res) == 2 and w.mip is None and w.out_dim <= 8:
         out_g = ntc.decode(model, q, bins, leaky_slope=slope, out_dtype=dtype, gather="staged")
         err_g = np.abs(out_g.cpu().numpy().astype(np.float64) - ref).max()
