@@ -82,7 +82,7 @@ def unique_latent_bytes(w) -> int:
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_binned_clustered4k_hbm_traffic.md")
 DECODE_SOURCES = [os.path.join(ROOT, "paper_2608_27888_amd", "csrc", f)
-                  for f in ("ntc_decode_kernels.h", "ntc_decode_l2c16.hip")]
+                  for f in ("ntc_decode_kernels.h", "ntc_decode_launch.h", "ntc_decode_l2c16.hip")]
 
 
 def decode_source_hash() -> str:
@@ -192,6 +192,21 @@ def timed(fn, steps, warmup, torch):
     return (time.perf_counter() - t0) / steps
 
 
+def event_ms(fn, reps, warmup, stream, torch):
+    """Mean kernel time of fn in ms: HIP events recorded on `stream` around each of
+    `reps` calls, after `warmup` untimed calls."""
+    for _ in range(warmup):
+        fn()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for a, b in ev:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return float(np.mean([a.elapsed_time(b) for a, b in ev]))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -296,7 +311,8 @@ def main():
 
     # ---------------------------------------------------------------- decoder variants
     # The Sec. 4 setup's decoder (LeakyReLU, positional encoding, RGB rows) and
-    # its parts, on the same frame and bins: binned decode time of each.
+    # its parts, on the same frame and bins: binned decode kernel time of each
+    # (HIP events on the decode stream, as for the headline's decode_ms).
     variants = None
     if not args.no_compare and w.mip is None:
         # right after the headline (clocks settled), each with its own warm-up
@@ -315,9 +331,9 @@ def main():
                 list(ww.dims), torch.from_numpy(ww.params.view(np.int16)).to(dev),
                 model.tex_to_dec, ww.pe_octaves)
             ov = torch.empty((n, ww.out_dim), dtype=dt, device=dev)
-            variants[tag] = round(timed(lambda: ntc.decode(mv, q, bins, out=ov, stream=stream,
-                                                          leaky_slope=slope, out_dtype=dt),
-                                        reps, reps, torch) * 1e3, 4)
+            variants[tag] = round(event_ms(lambda: ntc.decode(mv, q, bins, out=ov, stream=stream,
+                                                             leaky_slope=slope, out_dtype=dt),
+                                           reps, reps, stream, torch), 4)
             del ov
         log(f"[bench] decode variants {variants}")
 

@@ -21,7 +21,7 @@
 // Inside a 64-query row the lanes that share a decoder id are ranked with a
 // ballot and a lane count, one pass per distinct id of the row, so the order
 // inside a bin is ascending query index and the permutation is unique.  With at
-// most 63 decoders the wave's counters (count) and cursors (place) live in one
+// most 64 decoders the wave's counters (count) and cursors (place) live in one
 // register, lane k holding decoder k's, and a row costs no LDS access; with more
 // they live in a wave-private LDS table.  A wave issues the id loads of a whole
 // batch, then all of its map lookups, before it uses any of them.  The decoder
@@ -42,7 +42,7 @@ constexpr int64_t kMaxHistWords = (int64_t)1 << 20;              // slice histog
 constexpr uint32_t kOutside = 0xFFFFFFFFu;                       // a lane past the slice
 constexpr int kScanThreads = 1024;                               // scan: threads per column
 constexpr int kScanPerThread = 8;                                // scan: slices per thread
-constexpr uint32_t kRegDecoders = kWave - 1;                     // register tables up to here
+constexpr uint32_t kRegDecoders = kWave;                         // register tables up to here
 
 static_assert(kTargetBlocks * kWavesPerBlock <= (int64_t)kScanThreads * kScanPerThread,
               "one scan pass covers every slice");
@@ -145,15 +145,28 @@ bins_count(const uint32_t *__restrict__ tex_id, uint32_t n,
   WaveTable<REG> h{0u, lds + w * cols};
   if constexpr (!REG)
     for (uint32_t i = lane; i < cols; i += kWave) h.lds[i] = 0;
+  // With the register table the invalid queries are counted apart, in a
+  // wave-uniform counter, so that all 64 lanes can hold decoders.
+  uint32_t invalid = 0;
   for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
     uint32_t d[kBatchRows];
     load_batch(tex_id, tex_to_dec, n_textures, n_decoders, n_decoders, base, sl.end, lane, d);
 #pragma unroll
-    for (int j = 0; j < kBatchRows; ++j) rank_row<REG, false>(d[j], h, lane);
+    for (int j = 0; j < kBatchRows; ++j) {
+      if constexpr (REG) {
+        const uint64_t bad = ballot(d[j] == n_decoders);
+        invalid += (uint32_t)__builtin_popcountll(bad);
+        rank_row<REG, false>(d[j] == n_decoders ? kOutside : d[j], h, lane);
+      } else {
+        rank_row<REG, false>(d[j], h, lane);
+      }
+    }
   }
   if constexpr (REG) {
     // the wave's table is its own: no workgroup barrier
-    if (lane < cols) hist[(size_t)lane * n_slices + b * kWavesPerBlock + w] = h.reg;
+    const size_t col = b * kWavesPerBlock + w;
+    if (lane < n_decoders) hist[(size_t)lane * n_slices + col] = h.reg;
+    if (lane == 0) hist[(size_t)n_decoders * n_slices + col] = invalid;
   } else {
     // the workgroup's kWavesPerBlock slices are neighbours in every row of hist:
     // thread t writes row t / 4, slice t % 4, so a wave covers 16 rows with
