@@ -37,7 +37,8 @@ def _noalloc(tex_id, t2d, D, align, dev):
 
 
 @pytest.mark.parametrize("sizes", [((1_000_003, 512, 16, 64, 0), (70_001, 64, 7, 64, 3)),
-                                   ((300_000, 40, 33, 256, 11), (5_000, 40, 33, 128, 0))])
+                                   ((300_000, 40, 33, 256, 11), (5_000, 40, 33, 128, 0)),
+                                   ((8_294_400, 512, 16, 64, 5), (2_000_000, 64, 63, 64, 0))])
 def test_noalloc_matches_workspace_path(sizes):
     dev = torch.device("cuda:0")
     for k, (n, T, D, align, n_bad) in enumerate(sizes):
