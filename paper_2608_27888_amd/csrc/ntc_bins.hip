@@ -6,18 +6,25 @@
 // binning itself is not in the paper.
 //
 // The unit of the sort is one wave's contiguous slice of the query stream
-// (slice g = workgroup * 4 + wave), processed in batches of kBatchRows rows of
-// 64 queries.  Three kernels:
+// (slice g = workgroup * waves + wave), processed in batches of kBatchRows rows
+// of 64 queries.
+//
+// Up to 64 decoders, two kernels on workgroups of 16 waves:
 //   count : every wave resolves the decoder id of each query of its slice
-//           (tex_to_dec[tex_id[q]]) and counts the ids, which become column g
-//           of hist[d][g]; row D counts invalid queries.
-//   scan  : workgroup d turns row d into its exclusive prefix over slices, in
-//           place, and writes bin_count[d] (row D: the invalid count).
-//   place : every workgroup first scans bin_count into the padded bin offsets
-//           (workgroup 0 writes bin_offset, the padding slots are shared out
-//           among the workgroups); then each wave resolves the ids of its slice
-//           again and writes every query to the next slot of its bin, with
-//           cursors starting at bin_offset[d] + hist[d][g].
+//           (tex_to_dec[tex_id[q]]) and counts the ids; the workgroup writes its
+//           sums over its waves, column b of tot[d][b] (row D: invalid
+//           queries), and for slice g its waves' exclusive prefix, hist[d][g].
+//   place : every workgroup sums the rows of tot (at most 512 words each): the
+//           totals give the padded bin offsets (workgroup 0 writes bin_count
+//           and bin_offset, the padding slots are shared out among the
+//           workgroups), the columns before its own its offset inside every
+//           bin, and hist[d][g] each wave's offset after that.  Each wave then
+//           resolves the ids of its slice again and writes every query to the
+//           next slot of its bin.
+// With more decoders, three kernels on workgroups of 4 waves: count writes
+// hist only; scan (workgroup d) turns row d of hist into its exclusive prefix
+// over slices and writes bin_count[d]; place scans bin_count into the padded
+// offsets and starts its cursors at bin_offset[d] + hist[d][g].
 // Inside a 64-query row the lanes that share a decoder id are ranked with a
 // ballot and a lane count, one pass per distinct id of the row, so the order
 // inside a bin is ascending query index and the permutation is unique.  With at
@@ -36,8 +43,13 @@ namespace {
 
 constexpr int kBatchRows = 16;                                   // rows of 64 per wave batch
 constexpr int64_t kWaveQuantum = (int64_t)kWave * kBatchRows;    // queries per wave batch
-constexpr int64_t kChunkQuantum = kWaveQuantum * kWavesPerBlock;  // chunks are multiples of this
 constexpr int64_t kTargetBlocks = 2048;                          // workgroups, at most
+// The two-kernel path: workgroups of kSumWaves waves, at most kSumBlocks of
+// them, so that every place workgroup can sum the tot rows.
+constexpr int kSumWaves = 16;
+constexpr int64_t kSumBlocks = 512;
+constexpr int kSumLanes = 32;  // place: lanes per row of tot
+constexpr int kSumPer = 16;    // place: words of a row per lane
 constexpr int64_t kMaxHistWords = (int64_t)1 << 20;              // slice histograms, at most
 constexpr uint32_t kOutside = 0xFFFFFFFFu;                       // a lane past the slice
 constexpr int kScanThreads = 1024;                               // scan: threads per column
@@ -48,18 +60,20 @@ static_assert(kTargetBlocks * kWavesPerBlock <= (int64_t)kScanThreads * kScanPer
               "one scan pass covers every slice");
 
 // The workspace starts with kStatusWords status words -- [1] is the invalid
-// query count -- followed by hist[n_decoders + 1][slices].
+// query count -- followed by hist[n_decoders + 1][slices] and, on the
+// two-kernel path, tot[n_decoders + 1][workgroups].
 constexpr int kStatusWords = 4;
 
-// Query range [beg, end) of wave w of workgroup b.
+// Query range [beg, end) of wave w of a workgroup b of WAVES waves.
 struct Slice {
   uint64_t beg, end;
 };
 
+template <int WAVES>
 __device__ __forceinline__ Slice slice_of(uint32_t b, uint32_t w, uint64_t chunk, uint64_t n) {
   const uint64_t cbeg = (uint64_t)b * chunk;
   const uint64_t cend = cbeg + chunk < n ? cbeg + chunk : n;
-  const uint64_t wchunk = chunk / kWavesPerBlock;
+  const uint64_t wchunk = chunk / WAVES;
   const uint64_t beg = cbeg + w * wchunk < cend ? cbeg + w * wchunk : cend;
   return Slice{beg, beg + wchunk < cend ? beg + wchunk : cend};
 }
@@ -132,16 +146,21 @@ __device__ __forceinline__ uint32_t rank_row(uint32_t d, WaveTable<REG> &t, uint
   return pos;
 }
 
-template <bool REG>
-__global__ void __launch_bounds__(kBlock)
+// REG: register tables (n_decoders <= 64).  tot (REG only): the workgroup's
+// sums over its waves, column b of tot[n_decoders + 1][gridDim.x], with hist
+// holding each wave's exclusive prefix over the workgroup's waves; NULL: hist
+// holds each wave's own counts.
+template <bool REG, int WAVES>
+__global__ void __launch_bounds__(WAVES * kWave)
 bins_count(const uint32_t *__restrict__ tex_id, uint32_t n,
            const uint32_t *__restrict__ tex_to_dec, uint32_t n_textures, uint32_t n_decoders,
-           uint32_t chunk, uint32_t *__restrict__ hist) {
-  extern __shared__ uint32_t lds[];  // !REG: kWavesPerBlock x (n_decoders + 1) counters
+           uint32_t chunk, uint32_t *__restrict__ hist, uint32_t *__restrict__ tot) {
+  extern __shared__ uint32_t lds[];  // !REG: WAVES x (n_decoders + 1) counters
+  __shared__ uint32_t part[REG ? WAVES : 1][kWave + 1];
   const uint32_t b = xcd_local_block(blockIdx.x, gridDim.x), lane = lane_id();
   const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const uint32_t cols = n_decoders + 1, n_slices = gridDim.x * kWavesPerBlock;
-  const Slice sl = slice_of(b, w, chunk, n);
+  const uint32_t cols = n_decoders + 1, n_slices = gridDim.x * WAVES;
+  const Slice sl = slice_of<WAVES>(b, w, chunk, n);
   WaveTable<REG> h{0u, lds + w * cols};
   if constexpr (!REG)
     for (uint32_t i = lane; i < cols; i += kWave) h.lds[i] = 0;
@@ -163,18 +182,35 @@ bins_count(const uint32_t *__restrict__ tex_id, uint32_t n,
     }
   }
   if constexpr (REG) {
-    // the wave's table is its own: no workgroup barrier
-    const size_t col = b * kWavesPerBlock + w;
-    if (lane < n_decoders) hist[(size_t)lane * n_slices + col] = h.reg;
-    if (lane == 0) hist[(size_t)n_decoders * n_slices + col] = invalid;
+    const size_t col = b * WAVES + w;
+    if (!tot) {
+      if (lane < n_decoders) hist[(size_t)lane * n_slices + col] = h.reg;
+      if (lane == 0) hist[(size_t)n_decoders * n_slices + col] = invalid;
+    } else {
+      part[w][lane] = h.reg;
+      if (lane == 0) part[w][kWave] = invalid;
+      __syncthreads();
+      if (lane < n_decoders) {
+        uint32_t excl = 0;
+        for (uint32_t k = 0; k < w; ++k) excl += part[k][lane];
+        hist[(size_t)lane * n_slices + col] = excl;
+      }
+      if (threadIdx.x < cols) {
+        const uint32_t r = threadIdx.x < n_decoders ? threadIdx.x : kWave;
+        uint32_t sum = 0;
+#pragma unroll
+        for (int k = 0; k < WAVES; ++k) sum += part[k][r];
+        tot[(size_t)threadIdx.x * gridDim.x + b] = sum;
+      }
+    }
   } else {
-    // the workgroup's kWavesPerBlock slices are neighbours in every row of hist:
-    // thread t writes row t / 4, slice t % 4, so a wave covers 16 rows with
-    // 16-byte pieces
+    // the workgroup's WAVES slices are neighbours in every row of hist: thread
+    // t writes row t / WAVES, slice t % WAVES, so a wave covers 64 / WAVES rows
+    // with pieces of 4 WAVES bytes
     __syncthreads();
-    for (uint32_t i = threadIdx.x; i < cols * kWavesPerBlock; i += kBlock) {
-      const uint32_t r = i / kWavesPerBlock, ww = i % kWavesPerBlock;
-      hist[(size_t)r * n_slices + b * kWavesPerBlock + ww] = lds[ww * cols + r];
+    for (uint32_t i = threadIdx.x; i < cols * WAVES; i += WAVES * kWave) {
+      const uint32_t r = i / WAVES, ww = i % WAVES;
+      hist[(size_t)r * n_slices + b * WAVES + ww] = lds[ww * cols + r];
     }
   }
 }
@@ -238,7 +274,7 @@ bins_scan(uint32_t *__restrict__ hist, uint32_t n_slices, uint32_t n_decoders,
   }
 }
 
-template <bool REG>
+// Place of the three-kernel path (LDS tables).
 __global__ void __launch_bounds__(kBlock)
 bins_place(const uint32_t *__restrict__ tex_id, uint32_t n,
            const uint32_t *__restrict__ tex_to_dec, uint32_t n_textures, uint32_t n_decoders,
@@ -251,7 +287,7 @@ bins_place(const uint32_t *__restrict__ tex_id, uint32_t n,
   const uint32_t b = xcd_local_block(blockIdx.x, gridDim.x), lane = lane_id();
   const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const uint32_t nblocks = gridDim.x, n_slices = nblocks * kWavesPerBlock;
-  const Slice sl = slice_of(b, w, chunk, n);
+  const Slice sl = slice_of<kWavesPerBlock>(b, w, chunk, n);
   // The first batch's ids are in flight during the offset scan below; invalid
   // queries are marked as outside: they go nowhere.
   uint32_t d[kBatchRows];
@@ -284,14 +320,108 @@ bins_place(const uint32_t *__restrict__ tex_id, uint32_t n,
   }
   if (b == 0 && threadIdx.x == 0) bin_offset[D] = total;
   __syncthreads();
-  WaveTable<REG> cur{0u, lds + w * D};
-  if constexpr (REG) cur.reg = lane < D ? cur.lds[lane] : 0u;
+  WaveTable<false> cur{0u, lds + w * D};
   for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
     if (base != sl.beg)
       load_batch(tex_id, tex_to_dec, n_textures, D, kOutside, base, sl.end, lane, d);
 #pragma unroll
     for (int j = 0; j < kBatchRows; ++j) {
-      const uint32_t pos = rank_row<REG, true>(d[j], cur, lane);
+      const uint32_t pos = rank_row<false, true>(d[j], cur, lane);
+      if (d[j] != kOutside) perm[pos] = (uint32_t)(base + (uint64_t)j * kWave + lane);
+    }
+  }
+}
+
+// Place of the two-kernel path (register tables, n_decoders <= 64): the offsets
+// come from tot and from this workgroup's columns of hist.
+// Eight waves per SIMD: two workgroups of 16 waves per CU, so every
+// workgroup of a 4K frame is resident at once (the scalar registers decide).
+template <int WAVES>
+__global__ void __launch_bounds__(WAVES * kWave) __attribute__((amdgpu_waves_per_eu(8)))
+bins_place_sum(const uint32_t *__restrict__ tex_id, uint32_t n,
+               const uint32_t *__restrict__ tex_to_dec, uint32_t n_textures,
+               uint32_t n_decoders, uint32_t align, uint32_t chunk,
+               const uint32_t *__restrict__ hist, const uint32_t *__restrict__ tot,
+               uint32_t *__restrict__ bin_count, uint32_t *__restrict__ bin_offset,
+               uint32_t *__restrict__ perm, uint32_t *__restrict__ status,
+               uint32_t *__restrict__ invalid_out) {
+  __shared__ uint32_t total[kWave + 1], before[kWave + 1], start[kWave];
+  const uint32_t D = n_decoders;
+  const uint32_t b = xcd_local_block(blockIdx.x, gridDim.x), lane = lane_id();
+  const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const uint32_t nblocks = gridDim.x, n_slices = nblocks * WAVES;
+  const Slice sl = slice_of<WAVES>(b, w, chunk, n);
+  // The first batch's ids are in flight while the offsets are summed; invalid
+  // queries are marked as outside: they go nowhere.
+  uint32_t d[kBatchRows];
+  if (sl.beg < sl.end)
+    load_batch(tex_id, tex_to_dec, n_textures, D, kOutside, sl.beg, sl.end, lane, d);
+  // Row r of tot (r = D: invalid queries): its total and its sum over the
+  // workgroups before this one.  kSumLanes lanes take a row, kSumPer words
+  // each, all loaded at once.
+  static_assert(kSumLanes * kSumPer >= kSumBlocks, "a row fits its lanes");
+  for (uint32_t t = threadIdx.x; t < kSumLanes * (D + 1); t += WAVES * kWave) {
+    const uint32_t r = t / kSumLanes, i0 = (t % kSumLanes) * kSumPer;
+    const uint32_t *row = tot + (size_t)r * nblocks;
+    uint32_t v[kSumPer];
+#pragma unroll
+    for (int k = 0; k < kSumPer; ++k) v[k] = i0 + k < nblocks ? row[i0 + k] : 0u;
+    uint32_t all = 0, prior = 0;
+#pragma unroll
+    for (int k = 0; k < kSumPer; ++k) {
+      all += v[k];
+      prior += i0 + k < b ? v[k] : 0u;
+    }
+    // the kSumLanes lanes of a row are one aligned group, all active
+#pragma unroll
+    for (int sh = kSumLanes / 2; sh > 0; sh >>= 1) {
+      all += __shfl_xor(all, sh, kWave);
+      prior += __shfl_xor(prior, sh, kWave);
+    }
+    const uint32_t k = r < D ? r : kWave;
+    if (t % kSumLanes == 0) {
+      total[k] = all;
+      before[k] = prior;
+    }
+  }
+  __syncthreads();
+  if (w == 0) {
+    // padded bin offsets: lane k holds decoder k
+    const uint32_t cnt = lane < D ? total[lane] : 0u;
+    const uint32_t padded = (cnt + align - 1) & ~(align - 1);
+    uint32_t incl = padded;
+#pragma unroll
+    for (int s = 1; s < kWave; s <<= 1) {
+      const uint32_t o = __shfl_up(incl, s, kWave);
+      if (lane >= (uint32_t)s) incl += o;
+    }
+    const uint32_t off = incl - padded;
+    start[lane] = off;
+    if (b == 0) {
+      if (lane < D) {
+        bin_count[lane] = cnt;
+        bin_offset[lane] = off;
+      }
+      if (lane == kWave - 1) {
+        bin_offset[D] = incl;
+        status[1] = total[kWave];
+        if (invalid_out) *invalid_out = total[kWave];
+      }
+    }
+    if (lane < D && lane % nblocks == b)  // the padding slots of bin `lane`
+      for (uint32_t s = off + cnt; s < off + padded; ++s) perm[s] = NTC_PAD;
+  }
+  __syncthreads();
+  // this wave's cursor of decoder k (lane k): the bin's offset, the queries of
+  // the workgroups before this one, then those of this workgroup's earlier waves
+  WaveTable<true> cur{0u, nullptr};
+  if (lane < D) cur.reg = start[lane] + before[lane] + hist[(size_t)lane * n_slices + b * WAVES + w];
+  for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
+    if (base != sl.beg)
+      load_batch(tex_id, tex_to_dec, n_textures, D, kOutside, base, sl.end, lane, d);
+#pragma unroll
+    for (int j = 0; j < kBatchRows; ++j) {
+      const uint32_t pos = rank_row<true, true>(d[j], cur, lane);
       if (d[j] != kOutside) perm[pos] = (uint32_t)(base + (uint64_t)j * kWave + lane);
     }
   }
@@ -310,16 +440,21 @@ int allow_lds(const void *kernel, size_t bytes) {
 
 BinsLayout bins_layout(int64_t n, int32_t n_decoders) {
   BinsLayout L;
+  L.sum = (uint32_t)n_decoders <= kRegDecoders;
+  L.waves = L.sum ? kSumWaves : kWavesPerBlock;
   // fewer, longer slices for many decoders: the histograms stay within 4 MiB
-  int64_t max_blocks = kMaxHistWords / ((int64_t)kWavesPerBlock * (n_decoders + 1));
+  int64_t max_blocks = L.sum ? kSumBlocks
+                             : kMaxHistWords / ((int64_t)kWavesPerBlock * (n_decoders + 1));
   max_blocks = max_blocks < 1 ? 1 : max_blocks > kTargetBlocks ? kTargetBlocks : max_blocks;
+  const int64_t quantum = kWaveQuantum * L.waves;  // chunks are multiples of this
   int64_t chunk = (n + max_blocks - 1) / max_blocks;
-  chunk = (chunk + kChunkQuantum - 1) / kChunkQuantum * kChunkQuantum;
-  if (chunk < kChunkQuantum) chunk = kChunkQuantum;
+  chunk = (chunk + quantum - 1) / quantum * quantum;
+  if (chunk < quantum) chunk = quantum;
   L.chunk = chunk;
   L.blocks = n > 0 ? (n + chunk - 1) / chunk : 1;
-  L.hist_words = (size_t)(n_decoders + 1) * (size_t)L.blocks * kWavesPerBlock;
-  L.bytes = (kStatusWords + L.hist_words) * sizeof(uint32_t);
+  L.hist_words = (size_t)(n_decoders + 1) * (size_t)L.blocks * L.waves;
+  L.tot_words = L.sum ? (size_t)(n_decoders + 1) * (size_t)L.blocks : 0;
+  L.bytes = (kStatusWords + L.hist_words + L.tot_words) * sizeof(uint32_t);
   return L;
 }
 
@@ -331,32 +466,33 @@ int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_
   uint32_t *status = (uint32_t *)workspace;
   uint32_t *hist = status + kStatusWords;
   const uint32_t D = (uint32_t)n_decoders;
+  if (L.sum) {
+    uint32_t *tot = hist + L.hist_words;
+    const dim3 grid((unsigned)L.blocks), block(kSumWaves * kWave);
+    hipLaunchKernelGGL((bins_count<true, kSumWaves>), grid, block, 0, stream, tex_id, (uint32_t)n,
+                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist, tot);
+    hipLaunchKernelGGL(bins_place_sum<kSumWaves>, grid, block, 0, stream, tex_id, (uint32_t)n,
+                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk,
+                       hist, tot, bin_count, bin_offset, perm, status, invalid_out);
+    return hip_status(hipGetLastError());
+  }
   const uint32_t n_slices = (uint32_t)L.blocks * kWavesPerBlock;
-  const bool reg = D <= kRegDecoders;
-  const size_t lds_count = reg ? 0 : (size_t)kWavesPerBlock * (D + 1) * sizeof(uint32_t);
+  const size_t lds_count = (size_t)kWavesPerBlock * (D + 1) * sizeof(uint32_t);
   const size_t lds_place = (size_t)kWavesPerBlock * D * sizeof(uint32_t);
-  const void *count_fn = reg ? (const void *)bins_count<true> : (const void *)bins_count<false>;
-  const void *place_fn = reg ? (const void *)bins_place<true> : (const void *)bins_place<false>;
+  const void *count_fn = (const void *)bins_count<false, kWavesPerBlock>;
+  const void *place_fn = (const void *)bins_place;
   int st = allow_lds(count_fn, lds_count);
   if (st == NTC_OK) st = allow_lds(place_fn, lds_place);
   if (st != NTC_OK) return st;
   const dim3 grid((unsigned)L.blocks), block(kBlock);
-  if (reg)
-    hipLaunchKernelGGL(bins_count<true>, grid, block, lds_count, stream, tex_id, (uint32_t)n,
-                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist);
-  else
-    hipLaunchKernelGGL(bins_count<false>, grid, block, lds_count, stream, tex_id, (uint32_t)n,
-                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist);
+  hipLaunchKernelGGL((bins_count<false, kWavesPerBlock>), grid, block, lds_count, stream, tex_id,
+                     (uint32_t)n, tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist,
+                     nullptr);
   hipLaunchKernelGGL(bins_scan, dim3(D + 1), dim3(kScanThreads), 0, stream, hist, n_slices, D,
                      bin_count, status, invalid_out);
-  if (reg)
-    hipLaunchKernelGGL(bins_place<true>, grid, block, lds_place, stream, tex_id, (uint32_t)n,
-                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk,
-                       hist, bin_count, bin_offset, perm);
-  else
-    hipLaunchKernelGGL(bins_place<false>, grid, block, lds_place, stream, tex_id, (uint32_t)n,
-                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk,
-                       hist, bin_count, bin_offset, perm);
+  hipLaunchKernelGGL(bins_place, grid, block, lds_place, stream, tex_id, (uint32_t)n, tex_to_dec,
+                     (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk, hist, bin_count,
+                     bin_offset, perm);
   return hip_status(hipGetLastError());
 }
 

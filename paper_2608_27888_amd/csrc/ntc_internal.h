@@ -45,9 +45,12 @@ __device__ __forceinline__ uint32_t xcd_local_block(uint32_t b, uint32_t nblocks
 constexpr int64_t kMaxOutBytes = 0xFFFFFE00LL;
 
 struct BinsLayout {
+  bool sum;           // two kernels (n_decoders <= 64), else three
+  int waves;          // waves per workgroup
   int64_t chunk;      // queries per workgroup
   int64_t blocks;     // workgroups of the histogram / scatter kernels
-  size_t hist_words;  // (n_decoders + 1) * blocks
+  size_t hist_words;  // (n_decoders + 1) * blocks * waves
+  size_t tot_words;   // two kernels: (n_decoders + 1) * blocks
   size_t bytes;       // total workspace bytes
 };
 
