@@ -740,8 +740,12 @@ template <int HID, bool BINNED>
 constexpr int kWaves = BINNED || HID > 64 ? 8 : 4;
 template <int HID, bool BINNED>
 constexpr int kThreads = kWaves<HID, BINNED> * kWave;
-// Workgroups per CU the register allocation must allow, so that every SIMD
-// holds 4 waves of a 64-wide decoder (<= 128 VGPRs each) or 2 of a 128-wide one.
+// Minimum waves per SIMD the register allocation must allow (the second
+// argument of __launch_bounds__): 4 for the 64-wide stream kernels (<= 128
+// VGPRs), 2 for the 64-wide binned kernels and 1 for 128-wide decoders.  The
+// binned instantiation of the clustered workload takes 112 VGPRs (4 waves per
+// SIMD); asking for 4 there makes the fp16-output and mip-blending
+// instantiations spill.
 template <int HID, bool BINNED>
 constexpr int kMinBlocks = HID > 64 ? 1 : 16 / kWaves<HID, BINNED>;
 
