@@ -9,7 +9,8 @@
 // (slice g = workgroup * waves + wave), processed in batches of kBatchRows rows
 // of 64 queries.
 //
-// Up to 64 decoders, two kernels on workgroups of 16 waves:
+// Up to 64 decoders (while every workgroup can sum the rows of tot in two
+// rounds of loads), two kernels on workgroups of 4 to 16 waves:
 //   count : every wave resolves the decoder id of each query of its slice
 //           (tex_to_dec[tex_id[q]]) and counts the ids; the workgroup writes its
 //           sums over its waves, column b of tot[d][b] (row D: invalid
@@ -21,10 +22,10 @@
 //           bin, and hist[d][g] each wave's offset after that.  Each wave then
 //           resolves the ids of its slice again and writes every query to the
 //           next slot of its bin.
-// With more decoders, three kernels on workgroups of 4 waves: count writes
-// hist only; scan (workgroup d) turns row d of hist into its exclusive prefix
-// over slices and writes bin_count[d]; place scans bin_count into the padded
-// offsets and starts its cursors at bin_offset[d] + hist[d][g].
+// Otherwise three kernels on workgroups of 4 waves: count writes hist only;
+// scan (workgroup d) turns row d of hist into its exclusive prefix over slices
+// and writes bin_count[d]; place scans bin_count into the padded offsets and
+// starts its cursors at bin_offset[d] + hist[d][g].
 // Inside a 64-query row the lanes that share a decoder id are ranked with a
 // ballot and a lane count, one pass per distinct id of the row, so the order
 // inside a bin is ascending query index and the permutation is unique.  With at
@@ -44,12 +45,16 @@ namespace {
 constexpr int kBatchRows = 16;                                   // rows of 64 per wave batch
 constexpr int64_t kWaveQuantum = (int64_t)kWave * kBatchRows;    // queries per wave batch
 constexpr int64_t kTargetBlocks = 2048;                          // workgroups, at most
-// The two-kernel path: workgroups of kSumWaves waves, at most kSumBlocks of
-// them, so that every place workgroup can sum the tot rows.
-constexpr int kSumWaves = 16;
+// The two-kernel path: workgroups of 4, 8 or 16 waves, at most kSumBlocks of
+// them, so that every place workgroup can sum the tot rows.  The widest
+// workgroups that still give every CU one (kCus) keep many waves in flight on a
+// large frame; a smaller frame takes narrower ones, since the per-row ranking
+// runs on the CU's one scalar unit and a CU without a workgroup sits idle.
 constexpr int64_t kSumBlocks = 512;
+constexpr int64_t kCus = 256;
 constexpr int kSumLanes = 32;  // place: lanes per row of tot
 constexpr int kSumPer = 16;    // place: words of a row per lane
+constexpr int kSumRounds = 2;  // place: at most this many rounds of those loads
 constexpr int64_t kMaxHistWords = (int64_t)1 << 20;              // slice histograms, at most
 constexpr uint32_t kOutside = 0xFFFFFFFFu;                       // a lane past the slice
 constexpr int kScanThreads = 1024;                               // scan: threads per column
@@ -274,7 +279,8 @@ bins_scan(uint32_t *__restrict__ hist, uint32_t n_slices, uint32_t n_decoders,
   }
 }
 
-// Place of the three-kernel path (LDS tables).
+// Place of the three-kernel path.
+template <bool REG>
 __global__ void __launch_bounds__(kBlock)
 bins_place(const uint32_t *__restrict__ tex_id, uint32_t n,
            const uint32_t *__restrict__ tex_to_dec, uint32_t n_textures, uint32_t n_decoders,
@@ -320,13 +326,14 @@ bins_place(const uint32_t *__restrict__ tex_id, uint32_t n,
   }
   if (b == 0 && threadIdx.x == 0) bin_offset[D] = total;
   __syncthreads();
-  WaveTable<false> cur{0u, lds + w * D};
+  WaveTable<REG> cur{0u, lds + w * D};
+  if constexpr (REG) cur.reg = lane < D ? cur.lds[lane] : 0u;
   for (uint64_t base = sl.beg; base < sl.end; base += kWaveQuantum) {
     if (base != sl.beg)
       load_batch(tex_id, tex_to_dec, n_textures, D, kOutside, base, sl.end, lane, d);
 #pragma unroll
     for (int j = 0; j < kBatchRows; ++j) {
-      const uint32_t pos = rank_row<false, true>(d[j], cur, lane);
+      const uint32_t pos = rank_row<REG, true>(d[j], cur, lane);
       if (d[j] != kOutside) perm[pos] = (uint32_t)(base + (uint64_t)j * kWave + lane);
     }
   }
@@ -334,7 +341,7 @@ bins_place(const uint32_t *__restrict__ tex_id, uint32_t n,
 
 // Place of the two-kernel path (register tables, n_decoders <= 64): the offsets
 // come from tot and from this workgroup's columns of hist.
-// Eight waves per SIMD: two workgroups of 16 waves per CU, so every
+// Eight waves per SIMD (with 16-wave workgroups two per CU), so every
 // workgroup of a 4K frame is resident at once (the scalar registers decide).
 template <int WAVES>
 __global__ void __launch_bounds__(WAVES * kWave) __attribute__((amdgpu_waves_per_eu(8)))
@@ -427,6 +434,20 @@ bins_place_sum(const uint32_t *__restrict__ tex_id, uint32_t n,
   }
 }
 
+// The two kernels of the register-table path, on workgroups of WAVES waves.
+template <int WAVES>
+void launch_sum(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_dec,
+                int32_t n_textures, uint32_t D, int32_t align, const BinsLayout &L,
+                uint32_t *hist, uint32_t *tot, uint32_t *bin_count, uint32_t *bin_offset,
+                uint32_t *perm, uint32_t *status, uint32_t *invalid_out, hipStream_t stream) {
+  const dim3 grid((unsigned)L.blocks), block(WAVES * kWave);
+  hipLaunchKernelGGL((bins_count<true, WAVES>), grid, block, 0, stream, tex_id, (uint32_t)n,
+                     tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist, tot);
+  hipLaunchKernelGGL(bins_place_sum<WAVES>, grid, block, 0, stream, tex_id, (uint32_t)n,
+                     tex_to_dec, (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk,
+                     hist, tot, bin_count, bin_offset, perm, status, invalid_out);
+}
+
 // Lets a kernel use more than the default 64 KB of dynamic LDS.
 int allow_lds(const void *kernel, size_t bytes) {
   if (bytes + 64 <= 64 * 1024) return NTC_OK;
@@ -438,20 +459,35 @@ int allow_lds(const void *kernel, size_t bytes) {
 
 }  // namespace
 
-BinsLayout bins_layout(int64_t n, int32_t n_decoders) {
-  BinsLayout L;
-  L.sum = (uint32_t)n_decoders <= kRegDecoders;
-  L.waves = L.sum ? kSumWaves : kWavesPerBlock;
-  // fewer, longer slices for many decoders: the histograms stay within 4 MiB
-  int64_t max_blocks = L.sum ? kSumBlocks
-                             : kMaxHistWords / ((int64_t)kWavesPerBlock * (n_decoders + 1));
-  max_blocks = max_blocks < 1 ? 1 : max_blocks > kTargetBlocks ? kTargetBlocks : max_blocks;
-  const int64_t quantum = kWaveQuantum * L.waves;  // chunks are multiples of this
+// Workgroups and queries per workgroup for chunks of multiples of
+// kWaveQuantum * waves, at most max_blocks workgroups.
+static void split(BinsLayout &L, int64_t n, int64_t max_blocks) {
+  const int64_t quantum = kWaveQuantum * L.waves;
   int64_t chunk = (n + max_blocks - 1) / max_blocks;
   chunk = (chunk + quantum - 1) / quantum * quantum;
   if (chunk < quantum) chunk = quantum;
   L.chunk = chunk;
   L.blocks = n > 0 ? (n + chunk - 1) / chunk : 1;
+}
+
+BinsLayout bins_layout(int64_t n, int32_t n_decoders) {
+  BinsLayout L;
+  L.reg = (uint32_t)n_decoders <= kRegDecoders;
+  L.sum = false;
+  if (L.reg) {
+    // the two-kernel path while a place workgroup sums the tot rows in at most
+    // kSumRounds rounds of loads (kSumLanes threads per row)
+    L.waves = n >= kCus * 16 * kWaveQuantum ? 16 : n >= kCus * 8 * kWaveQuantum ? 8 : 4;
+    split(L, n, kSumBlocks);
+    L.sum = (int64_t)kSumLanes * (n_decoders + 1) <= (int64_t)kSumRounds * L.waves * kWave;
+  }
+  if (!L.sum) {
+    // fewer, longer slices for many decoders: the histograms stay within 4 MiB
+    L.waves = kWavesPerBlock;
+    int64_t max_blocks = kMaxHistWords / ((int64_t)kWavesPerBlock * (n_decoders + 1));
+    max_blocks = max_blocks < 1 ? 1 : max_blocks > kTargetBlocks ? kTargetBlocks : max_blocks;
+    split(L, n, max_blocks);
+  }
   L.hist_words = (size_t)(n_decoders + 1) * (size_t)L.blocks * L.waves;
   L.tot_words = L.sum ? (size_t)(n_decoders + 1) * (size_t)L.blocks : 0;
   L.bytes = (kStatusWords + L.hist_words + L.tot_words) * sizeof(uint32_t);
@@ -468,31 +504,45 @@ int launch_build_bins(const uint32_t *tex_id, int64_t n, const uint32_t *tex_to_
   const uint32_t D = (uint32_t)n_decoders;
   if (L.sum) {
     uint32_t *tot = hist + L.hist_words;
-    const dim3 grid((unsigned)L.blocks), block(kSumWaves * kWave);
-    hipLaunchKernelGGL((bins_count<true, kSumWaves>), grid, block, 0, stream, tex_id, (uint32_t)n,
-                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist, tot);
-    hipLaunchKernelGGL(bins_place_sum<kSumWaves>, grid, block, 0, stream, tex_id, (uint32_t)n,
-                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk,
-                       hist, tot, bin_count, bin_offset, perm, status, invalid_out);
+    if (L.waves == 16)
+      launch_sum<16>(tex_id, n, tex_to_dec, n_textures, D, align, L, hist, tot, bin_count,
+                     bin_offset, perm, status, invalid_out, stream);
+    else if (L.waves == 8)
+      launch_sum<8>(tex_id, n, tex_to_dec, n_textures, D, align, L, hist, tot, bin_count,
+                    bin_offset, perm, status, invalid_out, stream);
+    else
+      launch_sum<4>(tex_id, n, tex_to_dec, n_textures, D, align, L, hist, tot, bin_count,
+                    bin_offset, perm, status, invalid_out, stream);
     return hip_status(hipGetLastError());
   }
   const uint32_t n_slices = (uint32_t)L.blocks * kWavesPerBlock;
-  const size_t lds_count = (size_t)kWavesPerBlock * (D + 1) * sizeof(uint32_t);
+  const size_t lds_count = L.reg ? 0 : (size_t)kWavesPerBlock * (D + 1) * sizeof(uint32_t);
   const size_t lds_place = (size_t)kWavesPerBlock * D * sizeof(uint32_t);
-  const void *count_fn = (const void *)bins_count<false, kWavesPerBlock>;
-  const void *place_fn = (const void *)bins_place;
+  const void *count_fn = L.reg ? (const void *)bins_count<true, kWavesPerBlock>
+                               : (const void *)bins_count<false, kWavesPerBlock>;
+  const void *place_fn = L.reg ? (const void *)bins_place<true> : (const void *)bins_place<false>;
   int st = allow_lds(count_fn, lds_count);
   if (st == NTC_OK) st = allow_lds(place_fn, lds_place);
   if (st != NTC_OK) return st;
   const dim3 grid((unsigned)L.blocks), block(kBlock);
-  hipLaunchKernelGGL((bins_count<false, kWavesPerBlock>), grid, block, lds_count, stream, tex_id,
-                     (uint32_t)n, tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist,
-                     nullptr);
+  if (L.reg)
+    hipLaunchKernelGGL((bins_count<true, kWavesPerBlock>), grid, block, lds_count, stream, tex_id,
+                       (uint32_t)n, tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist,
+                       nullptr);
+  else
+    hipLaunchKernelGGL((bins_count<false, kWavesPerBlock>), grid, block, lds_count, stream, tex_id,
+                       (uint32_t)n, tex_to_dec, (uint32_t)n_textures, D, (uint32_t)L.chunk, hist,
+                       nullptr);
   hipLaunchKernelGGL(bins_scan, dim3(D + 1), dim3(kScanThreads), 0, stream, hist, n_slices, D,
                      bin_count, status, invalid_out);
-  hipLaunchKernelGGL(bins_place, grid, block, lds_place, stream, tex_id, (uint32_t)n, tex_to_dec,
-                     (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk, hist, bin_count,
-                     bin_offset, perm);
+  if (L.reg)
+    hipLaunchKernelGGL(bins_place<true>, grid, block, lds_place, stream, tex_id, (uint32_t)n,
+                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk,
+                       hist, bin_count, bin_offset, perm);
+  else
+    hipLaunchKernelGGL(bins_place<false>, grid, block, lds_place, stream, tex_id, (uint32_t)n,
+                       tex_to_dec, (uint32_t)n_textures, D, (uint32_t)align, (uint32_t)L.chunk,
+                       hist, bin_count, bin_offset, perm);
   return hip_status(hipGetLastError());
 }
 

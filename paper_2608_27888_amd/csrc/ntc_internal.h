@@ -45,7 +45,8 @@ __device__ __forceinline__ uint32_t xcd_local_block(uint32_t b, uint32_t nblocks
 constexpr int64_t kMaxOutBytes = 0xFFFFFE00LL;
 
 struct BinsLayout {
-  bool sum;           // two kernels (n_decoders <= 64), else three
+  bool reg;           // register tables (n_decoders <= 64), else LDS tables
+  bool sum;           // two kernels (register tables, tot rows small enough), else three
   int waves;          // waves per workgroup
   int64_t chunk;      // queries per workgroup
   int64_t blocks;     // workgroups of the histogram / scatter kernels

@@ -93,6 +93,38 @@ def test_bins_edge_sizes(dev, oracle, n):
     assert np.array_equal(u32(bins.perm)[: off[-1]], perm)
 
 
+@pytest.mark.parametrize("D", [1, 63, 64, 65])
+def test_bins_register_and_lds_paths(dev, oracle, D):
+    """Both sides of the 64-decoder boundary between the two-kernel path (register
+    tables) and the three-kernel path (LDS tables), over several workgroups with a
+    ragged last one, some ids out of range."""
+    rng = np.random.default_rng(900 + D)
+    T, n = 200, 3 * 16384 + 77
+    t2d = rng.integers(0, D + 1, T).astype(np.uint32)     # some textures map past D
+    tex = rng.integers(0, T + 2, n).astype(np.uint32)     # some ids past T
+    say(f"[bins-paths] D={D} n={n}")
+    bins = ntc.build_bins(torch.from_numpy(tex.view(np.int32)).to(dev),
+                          torch.from_numpy(t2d.view(np.int32)).to(dev), D, n_textures=T)
+    cnt, off, perm, bad = oracle.build_bins(tex, t2d, D, 64, n_textures=T)
+    assert np.array_equal(u32(bins.bin_count), cnt)
+    assert np.array_equal(u32(bins.bin_offset), off)
+    assert np.array_equal(u32(bins.perm)[: off[-1]], perm)
+    assert bad > 0 and ntc.device_error(bins) == bad
+
+
+@pytest.mark.parametrize("D", [16, 512])
+def test_bins_every_query_invalid(dev, oracle, D):
+    """No query lands in a bin: counts and offsets all zero, every query counted."""
+    n, T = 20001, 10
+    t2d = np.full(T, D, dtype=np.uint32)                  # every texture maps past D
+    tex = np.arange(n, dtype=np.uint32) % T
+    say(f"[bins-all-invalid] D={D}")
+    bins = ntc.build_bins(torch.from_numpy(tex.view(np.int32)).to(dev),
+                          torch.from_numpy(t2d.view(np.int32)).to(dev), D, n_textures=T)
+    assert not u32(bins.bin_count).any() and not u32(bins.bin_offset).any()
+    assert ntc.device_error(bins) == n
+
+
 @pytest.mark.parametrize("shift", [1, 2, 3])
 def test_bins_unaligned_ids(dev, oracle, shift):
     """tex_id that does not start on a 16-byte boundary (a slice of a larger array)."""
