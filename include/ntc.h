@@ -171,6 +171,25 @@ int ntc_build_bins_noalloc(const uint32_t *tex_id, int64_t n, const uint32_t *te
 int ntc_get_device_error(const void *workspace, uint64_t *n_invalid, void *stream);
 
 /*
+ * The feature vector of every query, without the MLP (the gather step of
+ * ntc_decode; Sec. 1 "latent pyramids or grids", sampled as described for
+ * ntc_queries): out[q][c] for c < F = n_levels * channels, row-major [n][F],
+ * slot l (level l, or the blend of the levels around max(l, mip)) at
+ * [l * channels, (l + 1) * channels).  The values are those ntc_decode feeds
+ * its MLP: bilinear weights rounded to fp16, every product and sum an fp16
+ * operation; out_format NTC_OUT_F32 widens them to float32 exactly,
+ * NTC_OUT_F16 stores them as fp16 bit patterns.  Rows of queries with
+ * tex_id >= n_textures are left untouched.
+ * Shapes as for ntc_decode: (n_levels, channels) in {(2, 8), (2, 16), (3, 16)},
+ * level resolutions in 2 .. 16384, latents of one texture < 2^31 values
+ * (NTC_ERR_UNSUPPORTED otherwise; malformed grids NTC_ERR_ARG).
+ * Alignment (NTC_ERR_ARG otherwise, when n > 0): latents and out 16 bytes, uv
+ * 8 bytes, tex_id and mip 4 bytes.
+ */
+int ntc_gather_features(const ntc_grids *grids, const ntc_queries *queries, void *out,
+                        int32_t out_format, void *stream);
+
+/*
  * Decode every query: out[q][c] = MLP_{d(q)}(features(q))[c], float32,
  * [n][dims[n_layers]] row-major, rows in original query order.
  *   Binned mode (bin_offset != NULL): queries are taken from `perm` in tiles of

@@ -119,6 +119,57 @@ int ntc_get_device_error(const void *workspace, uint64_t *n_invalid, void *strea
   return read_invalid_count(workspace, n_invalid, (hipStream_t)stream);
 }
 
+// Level layout of the grids into a: offsets, resolutions, values per texture,
+// latents and texture count (the level count is checked by the caller).
+static int set_grids(const ntc_grids *g, DecodeArgs &a) {
+  const int ch = g->channels[0];
+  int64_t tex_stride = 0;
+  for (int l = 0; l < g->n_levels; ++l) {
+    const int r = g->res[l];
+    if (r < 1 || r > 16384 || g->channels[l] < 1) return NTC_ERR_ARG;
+    if (r < 2) return NTC_ERR_UNSUPPORTED;  // the gather addresses a 2x2 quad
+    if (g->channels[l] != ch) return NTC_ERR_UNSUPPORTED;
+    a.level_off[l] = (uint32_t)tex_stride;
+    a.res[l] = r;
+    a.resf[l] = (float)r;
+    tex_stride += (int64_t)r * r * ch;
+    if (tex_stride >= ((int64_t)1 << 31)) return NTC_ERR_UNSUPPORTED;
+  }
+  a.latents = g->latents;
+  a.tex_stride = tex_stride;
+  a.n_textures = g->n_textures;
+  return NTC_OK;
+}
+
+int ntc_gather_features(const ntc_grids *g, const ntc_queries *q, void *out, int32_t out_format,
+                        void *stream) {
+  if (!g || !q) return NTC_ERR_ARG;
+  if (out_format != NTC_OUT_F32 && out_format != NTC_OUT_F16) return NTC_ERR_ARG;
+  if (q->n < 0 || q->n > kMaxQueries) return NTC_ERR_ARG;
+  if (g->n_textures < 1 || g->n_levels < 1 || g->n_levels > NTC_MAX_LEVELS) return NTC_ERR_ARG;
+  if (q->n > 0 && (!g->latents || !q->tex_id || !q->uv || !out)) return NTC_ERR_ARG;
+  // taps as 16-byte pieces, (u, v) as one 8-byte pair, rows as 16-byte pieces
+  if (q->n > 0 && (((uintptr_t)g->latents & 15) || ((uintptr_t)q->uv & 7) ||
+                   ((uintptr_t)q->tex_id & 3) || ((uintptr_t)q->mip & 3) ||
+                   ((uintptr_t)out & 15)))
+    return NTC_ERR_ARG;
+  DecodeArgs a = {};
+  const int gs = set_grids(g, a);
+  if (gs != NTC_OK) return gs;
+  a.tex_id = q->tex_id;
+  a.uv = q->uv;
+  a.mip = q->mip;
+  a.n = (uint32_t)q->n;
+  a.out = out;
+  if (q->n == 0) {
+    const int L = g->n_levels, ch = g->channels[0];
+    const bool known = (L == 2 && (ch == 8 || ch == 16)) || (L == 3 && ch == 16);
+    return known ? NTC_OK : NTC_ERR_UNSUPPORTED;
+  }
+  return launch_gather(a, g->n_levels, g->channels[0], out_format == NTC_OUT_F16,
+                       (hipStream_t)stream);
+}
+
 int ntc_decode(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex_to_dec,
                const ntc_queries *q, const uint32_t *bin_offset, const uint32_t *perm,
                int64_t perm_capacity, int32_t align, float *out, void *stream) {
@@ -169,19 +220,9 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
   // grid shape
   const int L = g->n_levels;
   const int ch = g->channels[0];
-  int64_t tex_stride = 0;
   DecodeArgs a = {};
-  for (int l = 0; l < L; ++l) {
-    const int r = g->res[l];
-    if (r < 1 || r > 16384 || g->channels[l] < 1) return NTC_ERR_ARG;
-    if (r < 2) return NTC_ERR_UNSUPPORTED;  // the gather addresses a 2x2 quad
-    if (g->channels[l] != ch) return NTC_ERR_UNSUPPORTED;
-    a.level_off[l] = (uint32_t)tex_stride;
-    a.res[l] = r;
-    a.resf[l] = (float)r;
-    tex_stride += (int64_t)r * r * ch;
-    if (tex_stride >= ((int64_t)1 << 31)) return NTC_ERR_UNSUPPORTED;
-  }
+  const int gs = set_grids(g, a);
+  if (gs != NTC_OK) return gs;
   // decoder shape: dims[0] = features, equal hidden widths, small output
   const int F = L * ch + 4 * o.pe_octaves;
   const int nl = m->n_layers;
@@ -199,9 +240,6 @@ int ntc_decode_ex(const ntc_grids *g, const ntc_decoders *m, const uint32_t *tex
   int64_t dec_stride = 0;
   for (int i = 0; i < nl; ++i) dec_stride += (int64_t)m->dims[i + 1] * (m->dims[i] + 1);
 
-  a.latents = g->latents;
-  a.tex_stride = tex_stride;
-  a.n_textures = g->n_textures;
   a.params = m->params;
   a.dec_stride = dec_stride;
   a.n_decoders = m->n_decoders;

@@ -109,6 +109,9 @@ struct DecodeArgs {
 // Returns NTC_ERR_UNSUPPORTED when no kernel is built for the shape.
 int launch_decode(const DecodeArgs &a, int n_levels, int channels, int feat, int hidden,
                   hipStream_t stream);
+// Feature rows of every query, fp32 or fp16 (ntc_gather_features); the same
+// shapes as launch_decode.
+int launch_gather(const DecodeArgs &a, int n_levels, int channels, bool f16, hipStream_t stream);
 // Per-lane vector-FMA decode in stream order (NTC_ENGINE_FMA); same contract.
 int launch_decode_fma(const DecodeArgs &a, int n_levels, int channels, int hidden,
                       hipStream_t stream);

@@ -76,6 +76,8 @@ def lib() -> ctypes.CDLL:
                                  ctypes.POINTER(Queries), P, P, i64, i32, P, P]
         L.ntc_decode_ex.argtypes = [ctypes.POINTER(Grids), ctypes.POINTER(Decoders), P,
                                     ctypes.POINTER(Queries), P, P, i64, i32, P, P, P]
+        L.ntc_gather_features.argtypes = [ctypes.POINTER(Grids), ctypes.POINTER(Queries), P, i32,
+                                          P]
         L.ntc_divergence_stats.argtypes = [P, i64, P, i32, i32, P, i64, i32, P, P, P]
         L.ntc_divergence_map.argtypes = [P, i32, i32, i32, P, i32, i32, i32, i32, P, P, i32, P, P]
         L.ntc_kmeans_workspace_bytes.argtypes = [i32, i32]
@@ -86,6 +88,7 @@ def lib() -> ctypes.CDLL:
         L.ntc_freeze_scale.argtypes = [d, d, d]
         L.ntc_freeze_scale.restype = d
         for f in ("ntc_build_bins", "ntc_build_bins_noalloc", "ntc_get_device_error", "ntc_decode", "ntc_decode_ex",
+                  "ntc_gather_features",
                   "ntc_divergence_stats", "ntc_divergence_map", "ntc_kmeans",
                   "ntc_kmeans_result"):
             getattr(L, f).restype = ctypes.c_int
@@ -320,6 +323,24 @@ def decode(model: DeviceModel, queries: DeviceQueries, bins: Optional[Bins] = No
                                  ctypes.byref(q), None, None, 0, 0, ctypes.byref(opt), _ptr(out),
                                  _stream(stream))
     _check("ntc_decode_ex", st)
+    return out
+
+
+def gather_features(model: DeviceModel, queries: DeviceQueries, out: Optional[torch.Tensor] = None,
+                    out_dtype: torch.dtype = torch.float32, stream=None) -> torch.Tensor:
+    """ntc_gather_features: the feature vector of every query (the decode's gather
+    step without the MLP), rows [n][n_levels * channels] of float32 or float16."""
+    if out_dtype not in (torch.float32, torch.float16):
+        raise ValueError("out_dtype must be float32 or float16")
+    F = sum(model.channels)
+    if out is None:
+        out = torch.empty((queries.n, F), dtype=out_dtype, device=queries.tex_id.device)
+    elif out.dtype != out_dtype:
+        raise ValueError("out has the wrong dtype")
+    g, q = model.grids(), queries.struct()
+    _check("ntc_gather_features", lib().ntc_gather_features(
+        ctypes.byref(g), ctypes.byref(q), _ptr(out),
+        NTC_OUT_F16 if out_dtype == torch.float16 else NTC_OUT_F32, _stream(stream)))
     return out
 
 

@@ -220,6 +220,52 @@ def test_decode_gather_validation(L):
             assert call(S, dims=dims, ch=ch) == ntc.NTC_ERR_HIP
 
 
+def test_gather_features_validation(L):
+    """ntc_gather_features: the decode's grid shapes, an output format, and
+    aligned pointers (latents and out 16 bytes, uv 8, tex_id and mip 4); with no
+    queries nothing is read."""
+    off = lambda b: ctypes.c_void_p(0x100000 + b)  # noqa: E731
+
+    def call(res=(256, 128), ch=(16, 16), fmt=ntc.NTC_OUT_F32, n=100, mip=False, ptrs=None,
+             n_textures=4):
+        p = {"latents": FAKE, "tex_id": FAKE, "uv": FAKE, "mip": FAKE if mip else None,
+             "out": FAKE}
+        p.update(ptrs or {})
+        g = ntc.Grids()
+        g.n_textures, g.n_levels = n_textures, len(res)
+        for i, (r, c) in enumerate(zip(res, ch)):
+            g.res[i], g.channels[i] = r, c
+        g.latents = p["latents"]
+        q = ntc.Queries()
+        q.tex_id, q.uv, q.mip, q.n = p["tex_id"], p["uv"], p["mip"], n
+        return L.ntc_gather_features(ctypes.byref(g), ctypes.byref(q), p["out"], fmt, None)
+
+    assert L.ntc_gather_features(None, None, FAKE, 0, None) == ntc.NTC_ERR_ARG
+    assert call(fmt=2) == ntc.NTC_ERR_ARG
+    assert call(fmt=-1) == ntc.NTC_ERR_ARG
+    assert call(n=-1) == ntc.NTC_ERR_ARG
+    assert call(n_textures=0) == ntc.NTC_ERR_ARG
+    assert call(res=(256, 0)) == ntc.NTC_ERR_ARG
+    assert call(ptrs={"out": None}) == ntc.NTC_ERR_ARG
+    assert call(ptrs={"uv": None}) == ntc.NTC_ERR_ARG
+    for b in (2, 4, 8):
+        assert call(ptrs={"latents": off(b)}) == ntc.NTC_ERR_ARG
+        assert call(ptrs={"out": off(b)}) == ntc.NTC_ERR_ARG
+    assert call(ptrs={"uv": off(4)}) == ntc.NTC_ERR_ARG
+    assert call(ptrs={"tex_id": off(2)}) == ntc.NTC_ERR_ARG
+    assert call(mip=True, ptrs={"mip": off(2)}) == ntc.NTC_ERR_ARG
+    # shapes the decode does not take
+    assert call(res=(256, 128), ch=(16, 8)) == ntc.NTC_ERR_UNSUPPORTED
+    assert call(res=(256, 1)) == ntc.NTC_ERR_UNSUPPORTED
+    assert call(res=(256,), ch=(16,)) == ntc.NTC_ERR_UNSUPPORTED
+    assert call(res=(256, 128), ch=(4, 4)) == ntc.NTC_ERR_UNSUPPORTED
+    assert call(res=(256, 128), ch=(4, 4), n=0) == ntc.NTC_ERR_UNSUPPORTED
+    for res, ch in (((256, 128), (16, 16)), ((64, 32), (8, 8)), ((512, 256, 128), (16,) * 3)):
+        assert call(res=res, ch=ch, n=0) == ntc.NTC_OK
+        if not HAS_DEVICE:  # accepted shapes reach the launch
+            assert call(res=res, ch=ch, fmt=ntc.NTC_OUT_F16, mip=True) == ntc.NTC_ERR_HIP
+
+
 def test_decode_options_validation(L):
     g = ntc.Grids()
     g.n_textures, g.n_levels = 4, 2
