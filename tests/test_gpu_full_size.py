@@ -3,7 +3,8 @@
 Binning, permutation and divergence counts are compared bit for bit with the
 oracle over the whole frame (the oracle's counting sort and window counts are
 cheap); decoded channels are compared on an evenly spaced sample of queries plus
-both ends of the frame, which the oracle decodes one by one in float64.  Every
+both ends of the frame, which the oracle decodes one by one in float64 (and the
+gather step's feature vectors on the same sample).  Every
 output row must be finite and in [0, 1], and the stream-order decode must equal
 the binned decode bit for bit on the whole frame.
 """
@@ -86,7 +87,18 @@ def check_frame(dev, oracle, w, n_sample, check_stream=True):
         say("    stream order vs binned")
         out_s = ntc.decode(model, q)
         assert torch.equal(out_s.view(torch.int32), out.view(torch.int32))
-    del model, q, bins, out
+        del out_s
+    # the gather step alone, on the same sample: within the fp16 arithmetic's
+    # bound of the oracle's features (see tests/test_gpu_gather.py)
+    feats = ntc.gather_features(model, q)
+    f_ref = oracle.features(w, subset=sub, pe_octaves=0)
+    f_err = np.abs(feats[torch.from_numpy(sub).to(dev)].cpu().numpy().astype(np.float64)
+                   - f_ref).max()
+    f_tol = (12.0 if w.mip is not None else 6.0) * 2.0 ** -11 \
+        * float(np.abs(W.bits_to_f32(w.latents)).max()) * 1.0001
+    say(f"    features: max abs err {f_err:.3e}, bound {f_tol:.3e}")
+    assert f_err <= f_tol
+    del model, q, bins, out, feats
     torch.cuda.empty_cache()
 
 
