@@ -141,11 +141,19 @@ __device__ __forceinline__ uint32_t rank_row(uint32_t d, WaveTable<REG> &t, uint
     const uint32_t leader = (uint32_t)__builtin_ctzll(todo);
     const uint32_t dl = read_lane(d, leader);
     const uint64_t same = ballot(d == dl) & todo;
-    if constexpr (RANK) {
-      const uint32_t at = t.get(dl);
-      pos = d == dl ? at + lanes_below(same) : pos;
+    const uint32_t c = (uint32_t)__builtin_popcountll(same);
+    if constexpr (RANK && !REG) {
+      // LDS table: the leader's returning atomic reads and advances the cursor
+      uint32_t old = 0;
+      if (lane == leader) old = atomicAdd(&t.lds[dl], c);
+      pos = d == dl ? read_lane(old, leader) + lanes_below(same) : pos;
+    } else {
+      if constexpr (RANK) {
+        const uint32_t at = t.get(dl);
+        pos = d == dl ? at + lanes_below(same) : pos;
+      }
+      t.add(dl, c, lane, lane == leader);
     }
-    t.add(dl, (uint32_t)__builtin_popcountll(same), lane, lane == leader);
     todo &= ~same;
   }
   return pos;
