@@ -761,10 +761,26 @@ decode_binned(const DecodeArgs a) {
   // tiles of the permutation; never more than the buffer holds
   const uint64_t slots = min((uint64_t)bin_off(a, D), a.perm_capacity);
   const uint32_t total_tiles = (uint32_t)(slots / kWave);
-  const uint32_t per = (total_tiles + gridDim.x - 1) / gridDim.x;
-  const uint32_t blk = xcd_local_block(blockIdx.x, gridDim.x);
-  const uint32_t t = blk * per;
-  const uint32_t t_end = min(t + per, total_tiles);
+  // This workgroup's contiguous range of tiles, in workgroups numbered XCD by
+  // XCD.  Equal ranges, or with a.split (two workgroups per CU, the grid a
+  // multiple of 16) twice the tiles for the first workgroup dispatched to each
+  // CU (blockIdx < gridDim / 2): the SIMDs issue the older waves first, so two
+  // co-resident workgroups with equal work finish a third apart and the second
+  // runs its last third on half the waves.
+  uint32_t t, t_end;
+  if (a.split) {
+    const uint32_t per_xcd = gridDim.x / 8, half = per_xcd / 2;
+    const uint32_t xcd = blockIdx.x % 8, j = blockIdx.x / 8;  // j < half: first on its CU
+    const uint64_t w0 = (uint64_t)xcd * half * 3 + (j < half ? 2 * j : 2 * half + (j - half));
+    const uint64_t w1 = w0 + (j < half ? 2 : 1);
+    const uint64_t W = (uint64_t)gridDim.x / 2 * 3;
+    t = (uint32_t)(total_tiles * w0 / W);
+    t_end = (uint32_t)(total_tiles * w1 / W);
+  } else {
+    const uint32_t per = (total_tiles + gridDim.x - 1) / gridDim.x;
+    t = xcd_local_block(blockIdx.x, gridDim.x) * per;
+    t_end = min(t + per, total_tiles);
+  }
   if (t >= t_end) return;
   // bin holding slot 64 t: the last d with bin_offset[d] <= 64 t
   uint32_t lo = 0, hi = D;  // invariant: bin_offset[lo] <= 64 t < bin_offset[hi]

@@ -104,6 +104,7 @@ struct DecodeArgs {
   int32_t pe_octaves;                 // positional-encoding octaves (0: none)
   int32_t gather;                     // NTC_GATHER_DIRECT or NTC_GATHER_STAGED
   int32_t fma_cache;                  // FMA engine: weights through the LDS decoder cache
+  uint32_t split;                     // binned: 2:1 tile ranges for a CU's two workgroups
 };
 
 // Returns NTC_ERR_UNSUPPORTED when no kernel is built for the shape.
