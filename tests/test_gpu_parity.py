@@ -125,6 +125,37 @@ def test_bins_every_query_invalid(dev, oracle, D):
     assert ntc.device_error(bins) == n
 
 
+def _bins_inputs(seed, n, T, D):
+    rng = np.random.default_rng(seed)
+    t2d = rng.integers(0, D + 1, T).astype(np.uint32)     # some textures map past D
+    # runs of one texture (screen-coherent regions) with some ids past T
+    runs = rng.integers(1, 300, n // 50 + 2)
+    ids = rng.integers(0, T + 2, runs.size).astype(np.uint32)
+    tex = np.repeat(ids, runs)[:n]
+    if tex.size < n:
+        tex = np.concatenate([tex, rng.integers(0, T, n - tex.size).astype(np.uint32)])
+    return tex, t2d
+
+
+@pytest.mark.parametrize("n,D", [(1_000_003, 15), (3_000_017, 16), (8_388_608, 64),
+                                 (8_388_609, 5)])
+def test_bins_workgroup_shapes(dev, oracle, n, D):
+    """Binning at 4-, 8- and 16-wave workgroups (two kernels), at the last size
+    where every wave's slice is one batch of 1024 queries (8,388,608; with 64
+    decoders the three-kernel path) and one past it, with runs of one texture
+    and some ids out of range."""
+    T = 300
+    tex, t2d = _bins_inputs(4000 + n % 1000, n, T, D)
+    say(f"[bins-shapes] n={n} D={D}")
+    bins = ntc.build_bins(torch.from_numpy(tex.view(np.int32)).to(dev),
+                          torch.from_numpy(t2d.view(np.int32)).to(dev), D, n_textures=T)
+    cnt, off, perm, bad = oracle.build_bins(tex, t2d, D, 64, n_textures=T)
+    assert np.array_equal(u32(bins.bin_count), cnt)
+    assert np.array_equal(u32(bins.bin_offset), off)
+    assert np.array_equal(u32(bins.perm)[: off[-1]], perm)
+    assert bad > 0 and ntc.device_error(bins) == bad
+
+
 @pytest.mark.parametrize("shift", [1, 2, 3])
 def test_bins_unaligned_ids(dev, oracle, shift):
     """tex_id that does not start on a 16-byte boundary (a slice of a larger array)."""
