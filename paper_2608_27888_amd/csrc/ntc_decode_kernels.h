@@ -704,10 +704,12 @@ __device__ __forceinline__ uint32_t bin_off(const DecodeArgs &a, uint32_t i) {
   return ((const_u32p)a.bin_offset)[i];
 }
 
-// A group of up to four consecutive tiles of one bin: tiles [t, t + n) of bin d,
-// whose tiles end at be.  n == 0 marks the end of a workgroup's range.
+// A group of up to WAVES consecutive tiles of one bin: tiles [t, t + n) of bin
+// d, whose tiles end at be; r counts the groups of a weighted sequence.  n == 0
+// marks the end of a workgroup's range.
 struct Group {
   uint32_t t, n, d, be;
+  uint32_t r = 0;
 };
 
 template <int WAVES>
@@ -726,6 +728,31 @@ template <int WAVES>
 __device__ __forceinline__ Group next_group(const DecodeArgs &a, const Group &g, uint32_t D,
                                             uint32_t t_end) {
   return g.n ? group_at<WAVES>(a, g.t + g.n, g.d, g.be, D, t_end) : g;
+}
+
+// Weighted groups: after every kRounds groups of up to WAVES tiles, one of up
+// to WAVES / 2 tiles, for the first half of the waves only, so that the first
+// half takes kRounds + 1 tiles for every kRounds of the second.  Waves w and
+// w + WAVES / 2 of a workgroup share a SIMD, which issues the older wave, w,
+// first.  Used by the binned decode of 128-wide decoders (2.61 -> 2.53 ms on
+// the 4-sample trilinear 4K frame); with 64-wide ones it gained nothing on the
+// 4K clustered frame and cost 2-4 % with positional encoding.
+constexpr uint32_t kRounds = 6;
+
+template <int WAVES>
+__device__ __forceinline__ Group wgroup_at(const DecodeArgs &a, uint32_t t, uint32_t d,
+                                           uint32_t be, uint32_t D, uint32_t t_end, uint32_t r) {
+  Group g = group_at<WAVES>(a, t, d, be, D, t_end);
+  if (r == kRounds) g.n = min(g.n, (uint32_t)WAVES / 2);
+  g.r = r;
+  return g;
+}
+
+template <int WAVES>
+__device__ __forceinline__ Group next_wgroup(const DecodeArgs &a, const Group &g, uint32_t D,
+                                             uint32_t t_end) {
+  return g.n ? wgroup_at<WAVES>(a, g.t + g.n, g.d, g.be, D, t_end, g.r == kRounds ? 0u : g.r + 1)
+             : g;
 }
 
 // Waves per workgroup.  The staged decoder is shared by a workgroup's waves.
@@ -788,13 +815,21 @@ decode_binned(const DecodeArgs a) {
     const uint32_t mid = (lo + hi) / 2;
     if (bin_off(a, mid) <= t * kWave) lo = mid; else hi = mid;
   }
-  // Tiles go in groups of up to four consecutive tiles of one bin, tile t + w to
-  // wave w; every wave walks the same (uniform) sequence of groups.  A wave
-  // without a tile in a group runs it with every lane masked.
+  // Tiles go in groups of consecutive tiles of one bin (weighted for 128-wide
+  // decoders), tile t + w to wave w; every wave walks the same (uniform)
+  // sequence of groups.  A wave without a tile in a group runs it with every
+  // lane masked, or, weighted, skips its MLP and stores but still takes part in
+  // its staging and prefetches.
+  constexpr bool WEIGHTED = HID > 64;
+  const uint32_t wu = __builtin_amdgcn_readfirstlane(w);
+  auto advance = [&](const Group &g) {
+    if constexpr (WEIGHTED) return next_wgroup<WAVES>(a, g, D, t_end);
+    else return next_group<WAVES>(a, g, D, t_end);
+  };
   Group g0 = group_at<WAVES>(a, t, lo, bin_off(a, lo + 1) / kWave, D, t_end);
-  Group g1 = next_group<WAVES>(a, g0, D, t_end);
-  Group g2 = next_group<WAVES>(a, g1, D, t_end);
-  Group g3 = next_group<WAVES>(a, g2, D, t_end);
+  Group g1 = advance(g0);
+  Group g2 = advance(g1);
+  Group g3 = advance(g2);
   // perm entry of this wave's tile in group g.  The load is unconditional (slot
   // 0 exists whenever there is a tile) and the entry stays raw until it is
   // used, with `has` saying whether the wave has a tile in the group: selecting
@@ -841,20 +876,24 @@ decode_binned(const DecodeArgs a) {
   // prefetch query data of the tile after from p_in into q_out and the
   // permutation entry of the tile after that into p_out, then store.
   auto tile = [&](const Query &q_in, const Slot &p_in, Query &q_out, Slot &p_out) {
-    uint32_t x[S::F / 2];
-    if constexpr (MIP)
-      gather<NL, CH, PE, MIP>(a, cur, x);
-    else {
-      interp_taps<NL, CH, PE>(taps, x);
-      if constexpr (PE > 0) pos_encoding<PE>(cur.u, cur.v, x + NL * CH / 2);
+    const bool busy = !WEIGHTED || wu < g0.n;  // this wave has a tile in the group
+    OutRows r0, r1;
+    if (busy) {
+      uint32_t x[S::F / 2];
+      if constexpr (MIP)
+        gather<NL, CH, PE, MIP>(a, cur, x);
+      else {
+        interp_taps<NL, CH, PE>(taps, x);
+        if constexpr (PE > 0) pos_encoding<PE>(cur.u, cur.v, x + NL * CH / 2);
+      }
+      half8 xb0[S::KS0], xb1[S::KS0];
+      to_b_operands<S::KS0>(x, xb0, xb1);
+      floatx16 z0, z1;
+      run_mlp<NL, CH, PE, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
+      const OutBias ob = load_out_bias<NL, CH, PE, HID, NH, STORE>(lds, a.out_dim);
+      r0 = finish_rows<STORE>(z0, ob, a.out_dim);
+      r1 = finish_rows<STORE>(z1, ob, a.out_dim);
     }
-    half8 xb0[S::KS0], xb1[S::KS0];
-    to_b_operands<S::KS0>(x, xb0, xb1);
-    floatx16 z0, z1;
-    run_mlp<NL, CH, PE, HID, NH, LEAKY>(lds, xb0, xb1, z0, z1, a.slope_h2);
-    const OutBias ob = load_out_bias<NL, CH, PE, HID, NH, STORE>(lds, a.out_dim);
-    const OutRows r0 = finish_rows<STORE>(z0, ob, a.out_dim);
-    const OutRows r1 = finish_rows<STORE>(z1, ob, a.out_dim);
     __builtin_amdgcn_sched_barrier(0);
     // The next group's decoder is staged here, between this tile's MLP and the
     // next tile's fetches, so no fetched data is live across the staging.
@@ -869,12 +908,12 @@ decode_binned(const DecodeArgs a) {
     q_out = load_query<NL, MIP>(a, p_in.raw, p_in.has);
     p_out = slot_query(g3);
     __builtin_amdgcn_sched_barrier(0);
-    store_tile<STORE>(out_rsrc, a.out_dim, cur.q, cur.valid, r0, r1, a.out_f16);
+    if (busy) store_tile<STORE>(out_rsrc, a.out_dim, cur.q, cur.valid, r0, r1, a.out_f16);
     cur = nxt;
     g0 = g1;
     g1 = g2;
     g2 = g3;
-    g3 = next_group<WAVES>(a, g3, D, t_end);
+    g3 = advance(g3);
   };
   // Unrolled by two with the prefetch registers swapping roles, so a fetched
   // value is never copied between registers (a copy would wait for the fetch).
