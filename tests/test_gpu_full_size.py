@@ -128,6 +128,17 @@ def test_full_clustered4k_d512(dev, oracle, clustered):
     check_frame(dev, oracle, w, 32768)
 
 
+@pytest.mark.parametrize("width,height", [(600, 400), (640, 420), (1100, 700)])
+def test_full_clustered_grid_fill(dev, oracle, width, height):
+    """Binned decode around the size where its grid fills every CU with two
+    workgroups (4096 tiles of 64 slots): 600x400 stays below it (equal tile
+    ranges), 640x420 just fills it and 1100x700 holds three times as many tiles
+    (the first workgroup on each CU then takes two thirds of the CU's tiles).
+    Binned equals stream bit for bit; the oracle on a sample."""
+    w = W.clustered4k(0, width, height, n_decoders=16, n_textures=64)
+    check_frame(dev, oracle, w, 32768)
+
+
 @pytest.fixture(scope="module")
 def wide(dev):
     return W.wide_trilinear()
