@@ -734,7 +734,7 @@ __device__ __forceinline__ Group next_group(const DecodeArgs &a, const Group &g,
 // to WAVES / 2 tiles, for the first half of the waves only, so that the first
 // half takes kRounds + 1 tiles for every kRounds of the second.  Waves w and
 // w + WAVES / 2 of a workgroup share a SIMD, which issues the older wave, w,
-// first.  Used by the binned decode of 128-wide decoders (2.61 -> 2.53 ms on
+// first.  Used by the binned decode of 128-wide decoders (2.64 -> 2.58 ms on
 // the 4-sample trilinear 4K frame); with 64-wide ones it gained nothing on the
 // 4K clustered frame and cost 2-4 % with positional encoding.
 constexpr uint32_t kRounds = 6;
